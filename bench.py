@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Benchmark: seconds per ACID-gated denoise loop at the Wan-2.1-1.3B shape.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One bench "step" is one whole denoise loop (timestep-modulation table, per
+step TEMNI + drift + gate, computed steps through all DiT blocks with the
+residual stored, skipped steps through the residual cache, head + Euler on
+every step) over one synthetic input.  W untimed loops, then K timed loops
+bracketed by device synchronisation; rank 0 prints one JSON line.
+
+Workload: 30 blocks, hidden 1536, 12 heads x 128, FFN 8960, 21 x 30 x 52 =
+32760 video tokens, batch 1, 50 flow-matching steps, ACID gate
+(tau_low 0.05, tau_high 0.2, delta 0.01), random-init weights N(0, 0.02^2)
+and N(0, 1) latents (synthetic stand-ins for the trained model and prompts).
+
+Per-kernel durations come from the library's HIP-event timer on the stream
+the kernels run on, over the timed loops.  The CPU baseline is the oracle
+(fp64 NumPy) timed on a bounded sample on this host and extrapolated.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "s per denoise loop; attention/GEMM TFLOP/s (% MFMA peak) at Wan-1.3B shape"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def work_per_class(cfg, n_computed: int, n_steps: int) -> dict:
+    """Algorithmic flops / bytes per kernel class for one loop (skipped work
+    not counted)."""
+    L, Lv, H, F, nb = cfg.n_tokens, cfg.n_video, cfg.hidden, cfg.ffn, cfg.n_blocks
+    es = 2 if cfg.dtype == "bf16" else 4
+    kc = n_computed
+    return {
+        "attention": ("flop", kc * nb * 4.0 * L * L * H),
+        "gemm_qkv": ("flop", kc * nb * 2.0 * L * H * 3 * H),
+        "gemm_proj": ("flop", kc * nb * 2.0 * L * H * H),
+        "gemm_ffn1": ("flop", kc * nb * 2.0 * L * H * F),
+        "gemm_ffn2": ("flop", kc * nb * 2.0 * L * F * H),
+        "gemm_head": ("flop", n_steps * 2.0 * Lv * H * H),
+        # TEMNI reads x, writes m; with a previous m also reads it (all fp32)
+        "drift": ("byte", (8.0 + 12.0 * (n_steps - 1)) * Lv * H),
+        # store: read x, h_out; write r.  apply: read x, r; write h_out.
+        "cache": ("byte", n_steps * 12.0 * Lv * H),
+        "ln_mod": ("byte", (kc * nb * 2 * L + n_steps * Lv) * H * (4.0 + es)),
+    }
+
+
+def cpu_baseline(ai, cfg, n_computed: int, n_steps: int, threads: int) -> dict:
+    """The oracle on a bounded sample: one DiT block (full keys/values, R query
+    rows at two values of R, extrapolated linearly to all rows), plus TEMNI,
+    drift and head on all video rows; scaled to seconds per loop with the GPU
+    run's computed-step count."""
+    import numpy as np
+
+    import oracle as O
+
+    c1 = cfg.replace(n_blocks=1)
+    params = ai.weights(c1)
+    om = O.DiTModel(c1, params)
+    x0 = ai.latents(cfg).astype(np.float64)
+    text = ai.text_tokens(cfg)
+    h = x0 if text is None else np.concatenate([text.astype(np.float64), x0])
+    mod = om.modulation(0.5)
+    L = h.shape[0]
+    ts = {}
+    for R in (64, 256):
+        rows = np.arange(R)
+        t0 = time.perf_counter()
+        om.block(h, 0, mod["blocks"][0], rows=rows)
+        ts[R] = time.perf_counter() - t0
+        log(f"cpu baseline: block with {R} query rows {ts[R]:.2f} s")
+    slope = (ts[256] - ts[64]) / (256 - 64)
+    t_block = ts[64] + slope * (L - 64)
+    t0 = time.perf_counter()
+    m_prev = om.temni(x0, 0.5)
+    m_cur = om.temni(x0 * 1.01, 0.48)
+    O.relative_l1_drift(m_cur, m_prev)
+    om.head(x0, 0.5)
+    t_every = time.perf_counter() - t0
+    log(f"cpu baseline: temni+drift+head {t_every:.2f} s")
+    s_loop = n_computed * cfg.n_blocks * t_block + n_steps * t_every
+    return {"value": s_loop, "unit": "s/loop", "cores": threads, "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle: one DiT block at full K/V for 64 and 256 query rows "
+                       f"(extrapolated linearly to {L} rows = {t_block:.1f} s/block), plus TEMNI, "
+                       f"drift and head on all {cfg.n_video} video rows ({t_every:.2f} s/step); "
+                       f"loop = {n_computed} computed steps x {cfg.n_blocks} blocks + {n_steps} "
+                       f"steps of per-step work (extrapolated)")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3, help="timed denoise loops")
+    ap.add_argument("--warmup", type=int, default=1, help="untimed denoise loops")
+    ap.add_argument("--workload", default="wan2.1-1.3b-shape")
+    ap.add_argument("--n-steps", type=int, default=None, help="denoising steps per loop")
+    ap.add_argument("--tau-low", type=float, default=0.05)
+    ap.add_argument("--tau-high", type=float, default=0.2)
+    ap.add_argument("--delta", type=float, default=0.01)
+    ap.add_argument("--no-nocache", action="store_true", help="skip the uncached context loop")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-timing", action="store_true", help="disable the per-kernel event timer")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the ACID-gated denoise loop here has no "
+              "multi-GPU path (no sharding, no collectives); use --gpus 1.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import acid_inputs as ai
+    import paper_2607_12358_amd as P
+
+    cfg = ai.CONFIGS[args.workload]
+    if args.n_steps:
+        cfg = cfg.replace(n_steps=args.n_steps)
+    N = cfg.n_steps
+    torch.cuda.set_device(0)
+    log(f"libacid {P.version()} on {torch.cuda.get_device_name(0)}; workload {cfg.name}")
+
+    t0 = time.perf_counter()
+    m = P.Model(cfg, max_steps=N)
+    m.load_weights(ai.iter_weights(cfg))
+    torch.cuda.synchronize()
+    log(f"weights generated and loaded in {time.perf_counter() - t0:.1f} s "
+        f"(arena {m.arena.numel() / 2**30:.2f} GiB, workspace {m.workspace.numel() / 2**30:.2f} GiB)")
+    x0 = torch.from_numpy(ai.latents(cfg)).cuda()
+    text = ai.text_tokens(cfg)
+    text_d = torch.from_numpy(text).cuda() if text is not None else None
+    sig = ai.sigmas(N)
+    x = torch.empty_like(x0)
+    gate = dict(tau_low=args.tau_low, tau_high=args.tau_high, delta=args.delta)
+
+    for w in range(args.warmup):
+        x.copy_(x0)
+        tr = m.denoise_loop(x, sig, text_d, mode="acid", **gate)
+        torch.cuda.synchronize()
+        log(f"warmup loop {w} done: {int(tr['compute'].sum())}/{N} computed")
+
+    if not args.no_timing:
+        m.reset_timing()
+        m.set_timing(True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    traces = []
+    for k in range(args.steps):
+        x.copy_(x0)
+        traces.append(m.denoise_loop(x, sig, text_d, mode="acid", **gate))
+        log(f"timed loop {k} issued")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    timing = m.timing() if not args.no_timing else {}
+    m.set_timing(False)
+    s_per_loop = elapsed / args.steps
+    n_comp = int(traces[-1]["compute"].sum())
+    assert all(np.array_equal(t["compute"], traces[0]["compute"]) for t in traces)
+    log(f"{args.steps} loops in {elapsed:.3f} s -> {s_per_loop:.3f} s/loop, {n_comp}/{N} computed")
+
+    # per-kernel-class rates over the timed region
+    work = work_per_class(cfg, n_comp, N)
+    kernels = {}
+    for name, (ms, launches) in timing.items():
+        if launches == 0:
+            continue
+        ent = {"ms_per_loop": ms / args.steps, "launches_per_loop": launches / args.steps,
+               "avg_us": 1e3 * ms / launches}
+        if name in work:
+            kind, amount = work[name]
+            rate = amount * args.steps / (ms * 1e-3)
+            if kind == "flop":
+                ent["tflops"] = rate / 1e12
+                ent["frac_bf16_peak"] = rate / 1e12 / PEAK_BF16_TFLOPS
+            else:
+                ent["gbs"] = rate / 1e9
+                ent["frac_hbm_peak"] = rate / 1e9 / PEAK_HBM_GBS
+        kernels[name] = ent
+    gemm_ms = sum(timing[k][0] for k in timing if k.startswith("gemm_"))
+    gemm_flop = sum(work[k][1] for k in work if k.startswith("gemm_"))
+    gemm_tflops = gemm_flop * args.steps / (gemm_ms * 1e-3) / 1e12 if gemm_ms else None
+
+    roofline = None
+    if "attention" in kernels:
+        L, H = cfg.n_tokens, cfg.hidden
+        per_launch = 4.0 * L * L * H
+        avg_s = kernels["attention"]["avg_us"] * 1e-6
+        ach = per_launch / avg_s / 1e12
+        roofline = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": ach / PEAK_BF16_TFLOPS, "traffic": None,
+                    "kernel": "attn_bf16_kernel<128>", "flop_per_launch": per_launch,
+                    "avg_launch_us": avg_s * 1e6}
+
+    nocache = None
+    if not args.no_nocache:
+        x.copy_(x0)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        m.denoise_loop(x, sig, text_d, mode="nocache")
+        torch.cuda.synchronize()
+        nocache = time.perf_counter() - t1
+        log(f"uncached loop: {nocache:.3f} s ({N} computed steps)")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max((i.get("num_threads", 1) for i in threadpool_info()
+                           if i.get("user_api") == "blas"), default=1)
+        except Exception:
+            threads = len(os.sched_getaffinity(0))
+        cpu = cpu_baseline(ai, cfg, n_comp, N, threads)
+
+    out = {
+        "metric": METRIC,
+        "value": s_per_loop,
+        "unit": "s/loop",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * s_per_loop,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "n_blocks": cfg.n_blocks, "hidden": cfg.hidden,
+                   "heads": cfg.n_heads, "head_dim": cfg.head_dim, "ffn": cfg.ffn,
+                   "video_tokens": cfg.n_video, "text_tokens": cfg.n_text, "batch": 1,
+                   "denoise_steps": N, "gate": {"mode": "acid", **gate, "n_warmup": 1},
+                   "parallelism": "single-gpu"},
+        "computed_steps": n_comp,
+        "schedule": "".join("C" if c else "S" for c in traces[-1]["compute"]),
+        "gemm_tflops": gemm_tflops,
+        "gemm_frac_bf16_peak": gemm_tflops / PEAK_BF16_TFLOPS if gemm_tflops else None,
+        "kernels": kernels,
+        "nocache_s_per_loop": nocache,
+        "speedup_vs_nocache": (nocache / s_per_loop) if nocache else None,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

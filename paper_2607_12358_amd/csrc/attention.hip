@@ -1,0 +1,320 @@
+// Full non-causal multi-head self-attention over all video (and text) tokens.
+//
+// bf16 path: flash-style single pass on MFMA (v_mfma_f32_32x32x16_bf16).
+//   A workgroup owns 128 queries of one head (4 waves x 32 queries) and
+//   streams the head's keys in tiles of 64 through LDS, double-buffered with
+//   register prefetch.  Scores are formed transposed, S^T = K Q^T, so that a
+//   lane owns one query (lane % 32) and 16 keys per 32-key block: the row max
+//   is an in-register max plus one exchange with the partner half-wave, and
+//   the row sum stays a per-lane partial until the end.  The probabilities
+//   P^T in accumulator layout are exactly the B operand of O^T = V^T P^T when
+//   the contraction index is relabelled accordingly, so P never leaves
+//   registers; V is stored transposed (keys contiguous) by the QKV epilogue
+//   so the matching A operand is two 8-byte LDS reads.  Softmax runs in the
+//   exp2 domain with log2(e)/sqrt(d) folded into one multiply, in fp32.
+// fp32 path: one thread per query with K/V tiles in LDS, online softmax in
+//   fp32 (for the fp32 configuration).
+#include "common.h"
+
+namespace acid {
+
+namespace {
+
+constexpr int BQ = 128, BKV = 64;
+
+template <int D>
+struct AttnLds {
+  static constexpr int KLD = D + 8;     // K tile row stride (elements)
+  static constexpr int VLD = BKV + 8;   // V^T tile row stride
+  static constexpr int K_ELEMS = BKV * KLD;
+  static constexpr int V_ELEMS = D * VLD;
+  static constexpr size_t BYTES = (size_t)2 * (K_ELEMS + V_ELEMS) * sizeof(bf16);
+};
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restrict__ Q,
+                                                           const bf16* __restrict__ Kp,
+                                                           const bf16* __restrict__ Vt,
+                                                           int64_t L, int64_t vt_ld, int n_heads,
+                                                           bf16* __restrict__ O,
+                                                           float scale_log2) {
+  using Ld = AttnLds<D>;
+  constexpr int KLD = Ld::KLD, VLD = Ld::VLD;
+  constexpr int NK = D / 16;     // MFMA K-steps over the head dim
+  constexpr int ND = D / 32;     // 32-row blocks of O^T
+  constexpr int CPT = D / 32;    // 16-byte chunks per thread per tile
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  bf16* Ks = reinterpret_cast<bf16*>(smem);
+  bf16* Vs = Ks + 2 * Ld::K_ELEMS;
+
+  const int head = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int64_t qrow = (int64_t)blockIdx.x * BQ + wave * 32 + lr;
+
+  const bf16* Qh = Q + (int64_t)head * L * D;
+  const bf16* Kh = Kp + (int64_t)head * L * D;
+  const bf16* Vh = Vt + (int64_t)head * D * vt_ld;
+
+  bf16x8 qf[NK];
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) {
+    if (qrow < L)
+      qf[kk] = *reinterpret_cast<const bf16x8*>(Qh + qrow * D + kk * 16 + lg * 8);
+    else
+      for (int i = 0; i < 8; ++i) qf[kk][i] = (bf16)0.f;
+  }
+
+  f32x16 o[ND];
+#pragma unroll
+  for (int db = 0; db < ND; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  float m_run = -__builtin_inff(), l_run = 0.f;
+
+  uint4 rk[CPT], rv[CPT];
+  const uint4 zero4 = make_uint4(0, 0, 0, 0);
+  auto gload = [&](int64_t j0) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + 256 * i, row = c / (D / 8), cc = c % (D / 8);
+      const int64_t key = j0 + row;
+      rk[i] = key < L ? *reinterpret_cast<const uint4*>(Kh + key * D + cc * 8) : zero4;
+    }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + 256 * i, drow = c >> 3, cc = c & 7;
+      const int64_t key0 = j0 + cc * 8;
+      uint4 v = zero4;
+      if (key0 < L) {
+        v = *reinterpret_cast<const uint4*>(Vh + (int64_t)drow * vt_ld + key0);
+        const int64_t valid = L - key0;  // keys past L are zeroed
+        if (valid < 8) {
+          uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (e >= valid) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+          v = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+      }
+      rv[i] = v;
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + 256 * i, row = c / (D / 8), cc = c % (D / 8);
+      *reinterpret_cast<uint4*>(Ks + buf * Ld::K_ELEMS + row * KLD + cc * 8) = rk[i];
+    }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + 256 * i, drow = c >> 3, cc = c & 7;
+      *reinterpret_cast<uint4*>(Vs + buf * Ld::V_ELEMS + drow * VLD + cc * 8) = rv[i];
+    }
+  };
+
+  const int64_t nkv = (L + BKV - 1) / BKV;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int64_t it = 0; it < nkv; ++it) {
+    const int buf = (int)(it & 1);
+    const int64_t j0 = it * BKV;
+    if (it + 1 < nkv) gload(j0 + BKV);
+
+    // S^T (keys x queries) for two 32-key blocks.
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+      const bf16* kbase = Ks + buf * Ld::K_ELEMS + (kb * 32 + lr) * KLD + lg * 8;
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kbase + kk * 16);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+      }
+    }
+    // Scale into the exp2 domain, mask keys past L, row max.
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t key = j0 + kb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+        const float v = key < L ? s[kb][r] * scale_log2 : -__builtin_inff();
+        s[kb][r] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = exp2f(m_run - m_new);
+    m_run = m_new;
+    float psum = 0.f;
+    bf16x8 pf[2][2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = exp2f(s[kb][r] - m_new);
+        psum += p;
+        pf[kb][r >> 3][r & 7] = (bf16)p;
+      }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int db = 0; db < ND; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+
+    // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
+    // (kb, k2) is key kb*32 + 16 k2 + 8 (e / 4) + 4 lg + e % 4, matching the
+    // accumulator rows of S^T that became pf[kb][k2].
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      const bf16* vbase = Vs + buf * Ld::V_ELEMS + (db * 32 + lr) * VLD + 4 * lg;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int kb = ks >> 1, k2 = ks & 1;
+        const bf16* p = vbase + kb * 32 + k2 * 16;
+        bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
+        bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 8);
+        bf16x8 vf;
+        vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
+        vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][k2], o[db], 0, 0, 0);
+      }
+    }
+    if (it + 1 < nkv) sstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  const float inv = 1.0f / l_tot;
+  if (qrow < L) {
+    bf16* orow = O + qrow * ((int64_t)n_heads * D) + (int64_t)head * D;
+#pragma unroll
+    for (int db = 0; db < ND; ++db)
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        bf16x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = (bf16)(o[db][rg * 4 + e] * inv);
+        *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * rg + 4 * lg) = w;
+      }
+  }
+}
+
+// ------------------------------------------------------------------ fp32
+
+constexpr int FQ = 64, FKV = 32;
+
+template <int D>
+__global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ Q,
+                                                      const float* __restrict__ Kp,
+                                                      const float* __restrict__ Vt, int64_t L,
+                                                      int64_t vt_ld, int n_heads,
+                                                      float* __restrict__ O, float scale) {
+  __shared__ float Ks[FKV][D];
+  __shared__ float Vs[FKV][D + 1];
+  const int head = blockIdx.y;
+  const int t = threadIdx.x;
+  const int64_t qrow = (int64_t)blockIdx.x * FQ + t;
+  const float* Qh = Q + (int64_t)head * L * D;
+  const float* Kh = Kp + (int64_t)head * L * D;
+  const float* Vh = Vt + (int64_t)head * D * vt_ld;
+  float q[D], o[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    q[d] = qrow < L ? Qh[qrow * D + d] : 0.f;
+    o[d] = 0.f;
+  }
+  float m_run = -__builtin_inff(), l_run = 0.f;
+  for (int64_t j0 = 0; j0 < L; j0 += FKV) {
+    __syncthreads();
+    for (int idx = t; idx < FKV * D; idx += 64) {
+      const int j = idx / D, d = idx % D;
+      Ks[j][d] = (j0 + j < L) ? Kh[(j0 + j) * D + d] : 0.f;
+    }
+    for (int idx = t; idx < FKV * D; idx += 64) {
+      const int d = idx / FKV, j = idx % FKV;
+      Vs[j][d] = (j0 + j < L) ? Vh[(int64_t)d * vt_ld + j0 + j] : 0.f;
+    }
+    __syncthreads();
+    float sc[FKV];
+    float mx = -__builtin_inff();
+#pragma unroll
+    for (int j = 0; j < FKV; ++j) {
+      float a = 0.f;
+#pragma unroll
+      for (int d = 0; d < D; ++d) a += q[d] * Ks[j][d];
+      sc[j] = (j0 + j < L) ? a * scale : -__builtin_inff();
+      mx = fmaxf(mx, sc[j]);
+    }
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = expf(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int d = 0; d < D; ++d) o[d] *= alpha;
+#pragma unroll
+    for (int j = 0; j < FKV; ++j) {
+      const float p = expf(sc[j] - m_new);
+      l_run += p;
+#pragma unroll
+      for (int d = 0; d < D; ++d) o[d] += p * Vs[j][d];
+    }
+  }
+  if (qrow < L) {
+    const float inv = 1.0f / l_run;
+    float* orow = O + qrow * ((int64_t)n_heads * D) + (int64_t)head * D;
+#pragma unroll
+    for (int d = 0; d < D; ++d) orow[d] = o[d] * inv;
+  }
+}
+
+template <int D>
+hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
+                       int64_t vt_ld, void* o, hipStream_t s) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t err = hipFuncSetAttribute((const void*)attn_bf16_kernel<D>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         (int)AttnLds<D>::BYTES);
+    if (err != hipSuccess) return err;
+    attr_set = true;
+  }
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
+  dim3 grid((unsigned)((L + BQ - 1) / BQ), (unsigned)n_heads);
+  hipLaunchKernelGGL(attn_bf16_kernel<D>, grid, dim3(256), AttnLds<D>::BYTES, s,
+                     (const bf16*)q, (const bf16*)k, (const bf16*)vt, L, vt_ld, n_heads,
+                     (bf16*)o, scale_log2);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
+                      int64_t vt_ld, void* o, hipStream_t s) {
+  dim3 grid((unsigned)((L + FQ - 1) / FQ), (unsigned)n_heads);
+  hipLaunchKernelGGL(attn_f32_kernel<D>, grid, dim3(64), 0, s, (const float*)q,
+                     (const float*)k, (const float*)vt, L, vt_ld, n_heads, (float*)o,
+                     1.0f / sqrtf((float)D));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
+                            const void* k, const void* vt, int64_t vt_ld, void* o,
+                            hipStream_t s) {
+  if (L == 0) return hipSuccess;
+  if (dtype == ACID_BF16) {
+    if (d == 64) return launch_bf16<64>(n_heads, L, q, k, vt, vt_ld, o, s);
+    if (d == 128) return launch_bf16<128>(n_heads, L, q, k, vt, vt_ld, o, s);
+  } else {
+    if (d == 64) return launch_f32<64>(n_heads, L, q, k, vt, vt_ld, o, s);
+    if (d == 128) return launch_f32<128>(n_heads, L, q, k, vt, vt_ld, o, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace acid

@@ -1,0 +1,96 @@
+// Internal helpers of libacid (gfx950).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "acid.h"
+
+namespace acid {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Records a message for acid_last_error() and returns the status.
+acid_status set_error(acid_status st, const char* fmt, ...);
+acid_status check_hip(hipError_t e, const char* what);
+
+#define ACID_HIP(call)                                            \
+  do {                                                            \
+    hipError_t e_ = (call);                                       \
+    if (e_ != hipSuccess) return ::acid::check_hip(e_, #call);    \
+  } while (0)
+
+#define ACID_TRY(call)                          \
+  do {                                          \
+    acid_status s_ = (call);                    \
+    if (s_ != ACID_OK) return s_;               \
+  } while (0)
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float gelu_tanh(float z) {
+  // 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3)))
+  const float k0 = 0.7978845608028654f;
+  float u = k0 * (z + 0.044715f * z * z * z);
+  return 0.5f * z * (1.0f + tanhf(u));
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+
+inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
+
+// ---------------------------------------------------------------- launchers
+// Each returns hipGetLastError() of its launch.
+
+// Elementwise / row kernels (elementwise.hip)
+hipError_t launch_ln_modulate(int out_dtype, const float* x, int64_t rows, int H,
+                              const float* shift, const float* scale, void* out,
+                              hipStream_t s);
+// TEMNI + per-row partial sums; m_prev may be null (then no partials).
+hipError_t launch_temni_drift(const float* x, int64_t rows, int H, const float* shift,
+                              const float* scale, const float* m_prev, float* m_cur,
+                              double* partials, hipStream_t s);
+// Fixed-order reduction of per-row (num, den) pairs -> out[0]=num, out[1]=den, out[2]=s.
+hipError_t launch_drift_finalize(const double* partials, int64_t rows, double* out,
+                                 hipStream_t s);
+hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n,
+                        hipStream_t s);
+// fp32 [in][out] -> [out][in] in dtype
+hipError_t launch_transpose_convert(const float* src, int64_t in, int64_t out, int dtype,
+                                    void* dst, hipStream_t s);
+
+// Timestep embedding + modulation (temb.hip)
+// e[i][:] = [cos(t f_j)]_j ++ [sin(t f_j)]_j with t = 1000 sigmas_host[i], in fp64.
+hipError_t launch_sinusoid(const float* sigmas_host, int n, int freq_dim, float* e,
+                           hipStream_t s);
+// Y[s][n] = act_out( X[s][:] . W[:, n] + b[n] ) (act_out: 0 none, 1 SiLU), batched over `batch`
+// groups with element strides for W, b and the output column offset.
+hipError_t launch_skinny_gemm(const float* X, int ldx, int S, int K, const float* W,
+                              int N, const float* b, float* Y, int64_t ldy, int act_out,
+                              int batch, int64_t w_stride, int64_t b_stride,
+                              int64_t y_stride, hipStream_t s);
+
+// GEMMs (gemm.hip)
+hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, const void* wt,
+                         const acid_epilogue_args& epi, hipStream_t s);
+
+// Attention (attention.hip)
+hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
+                            const void* k, const void* vt, int64_t vt_ld, void* o,
+                            hipStream_t s);
+
+}  // namespace acid

@@ -1,0 +1,302 @@
+// Row-wise and elementwise kernels: LayerNorm + adaLN modulate, TEMNI +
+// relative-L1 drift partial sums, the fixed-order drift reduction, the
+// residual cache, and weight layout conversion.
+//
+// All are HBM-bound.  A row (hidden <= 4096 fp32) is owned by one 64-wide
+// wavefront and kept in registers as float4 chunks, so LayerNorm statistics
+// take two in-register passes (mean, then centred variance) and each row is
+// read from HBM exactly once.
+#include "common.h"
+
+namespace acid {
+
+namespace {
+
+constexpr int kRowsPerBlock = 4;  // 4 waves x 1 row
+
+__device__ __forceinline__ void store4(float* out, int64_t idx4, float4 y) {
+  reinterpret_cast<float4*>(out)[idx4] = y;
+}
+__device__ __forceinline__ void store4(bf16* out, int64_t idx4, float4 y) {
+  bf16x4 v;
+  v[0] = (bf16)y.x;
+  v[1] = (bf16)y.y;
+  v[2] = (bf16)y.z;
+  v[3] = (bf16)y.w;
+  reinterpret_cast<bf16x4*>(out)[idx4] = v;
+}
+
+// Loads a row into registers and returns (mean, rstd) of LayerNorm
+// (biased variance, eps 1e-6).
+template <int CPL>
+__device__ __forceinline__ void load_row_stats(const float4* __restrict__ xr, int n4, int lane,
+                                               float4 (&v)[CPL], float& mean, float& rstd,
+                                               int H) {
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    int idx = lane + 64 * c;
+    if (idx < n4) {
+      v[c] = *(xr + idx);
+      s += (v[c].x + v[c].y) + (v[c].z + v[c].w);
+    } else {
+      v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  s = wave_sum(s);
+  mean = s / (float)H;
+  float q = 0.f;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    int idx = lane + 64 * c;
+    if (idx < n4) {
+      float a = v[c].x - mean, b = v[c].y - mean, cc = v[c].z - mean, d = v[c].w - mean;
+      q += (a * a + b * b) + (cc * cc + d * d);
+    }
+  }
+  q = wave_sum(q);
+  rstd = 1.0f / sqrtf(q / (float)H + 1e-6f);
+}
+
+template <int CPL, typename OutT>
+__global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restrict__ x,
+                                                          int64_t rows, int H,
+                                                          const float* __restrict__ shift,
+                                                          const float* __restrict__ scale,
+                                                          OutT* __restrict__ out) {
+  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;  // whole wave leaves together
+  const int n4 = H >> 2;
+  float4 v[CPL];
+  float mean, rstd;
+  load_row_stats<CPL>(reinterpret_cast<const float4*>(x + row * H), n4, lane, v, mean, rstd, H);
+  const float4* sh4 = reinterpret_cast<const float4*>(shift);
+  const float4* sc4 = reinterpret_cast<const float4*>(scale);
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    int idx = lane + 64 * c;
+    if (idx < n4) {
+      float4 sc = sc4[idx], sh = sh4[idx], y;
+      y.x = (v[c].x - mean) * rstd * (1.f + sc.x) + sh.x;
+      y.y = (v[c].y - mean) * rstd * (1.f + sc.y) + sh.y;
+      y.z = (v[c].z - mean) * rstd * (1.f + sc.z) + sh.z;
+      y.w = (v[c].w - mean) * rstd * (1.f + sc.w) + sh.w;
+      store4(out, row * n4 + idx, y);
+    }
+  }
+}
+
+// TEMNI m = LN(x) (1 + scale) + shift, stored; if m_prev is given, each row
+// also writes (sum|m - m_prev|, sum|m_prev|) as doubles to partials[2 row].
+template <int CPL>
+__global__ __launch_bounds__(256) void temni_drift_kernel(
+    const float* __restrict__ x, int64_t rows, int H, const float* __restrict__ shift,
+    const float* __restrict__ scale, const float* __restrict__ m_prev,
+    float* __restrict__ m_cur, double* __restrict__ partials) {
+  const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const int n4 = H >> 2;
+  float4 v[CPL];
+  float mean, rstd;
+  load_row_stats<CPL>(reinterpret_cast<const float4*>(x + row * H), n4, lane, v, mean, rstd, H);
+  const float4* sh4 = reinterpret_cast<const float4*>(shift);
+  const float4* sc4 = reinterpret_cast<const float4*>(scale);
+  const float4* mp4 = reinterpret_cast<const float4*>(m_prev + row * H);
+  float4* mc4 = reinterpret_cast<float4*>(m_cur + row * H);
+  float num = 0.f, den = 0.f;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    int idx = lane + 64 * c;
+    if (idx < n4) {
+      float4 sc = sc4[idx], sh = sh4[idx], y;
+      y.x = (v[c].x - mean) * rstd * (1.f + sc.x) + sh.x;
+      y.y = (v[c].y - mean) * rstd * (1.f + sc.y) + sh.y;
+      y.z = (v[c].z - mean) * rstd * (1.f + sc.z) + sh.z;
+      y.w = (v[c].w - mean) * rstd * (1.f + sc.w) + sh.w;
+      if (m_prev) {
+        float4 p = *(mp4 + idx);
+        num += (fabsf(y.x - p.x) + fabsf(y.y - p.y)) + (fabsf(y.z - p.z) + fabsf(y.w - p.w));
+        den += (fabsf(p.x) + fabsf(p.y)) + (fabsf(p.z) + fabsf(p.w));
+      }
+      *(mc4 + idx) = y;
+    }
+  }
+  if (m_prev) {
+    num = wave_sum(num);
+    den = wave_sum(den);
+    if (lane == 0) {
+      partials[2 * row] = (double)num;
+      partials[2 * row + 1] = (double)den;
+    }
+  }
+}
+
+// One block of 1024 threads: thread t sums rows t, t+1024, ... in order, then
+// a fixed binary tree in LDS.  Deterministic for a given row count.
+__global__ __launch_bounds__(1024) void drift_finalize_kernel(const double* __restrict__ part,
+                                                              int64_t rows,
+                                                              double* __restrict__ out) {
+  __shared__ double sn[1024], sd[1024];
+  const int t = threadIdx.x;
+  double n = 0.0, d = 0.0;
+  for (int64_t r = t; r < rows; r += 1024) {
+    n += part[2 * r];
+    d += part[2 * r + 1];
+  }
+  sn[t] = n;
+  sd[t] = d;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if (t < w) {
+      sn[t] += sn[t + w];
+      sd[t] += sd[t + w];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    double num = sn[0], den = sd[0], s;
+    if (den == 0.0)
+      s = (num == 0.0) ? 0.0 : __builtin_inf();
+    else
+      s = num / den;
+    out[0] = num;
+    out[1] = den;
+    out[2] = s;
+  }
+}
+
+// STORE: r = h - x ; APPLY: h = x + r.  float4 body, scalar tail.
+template <int OP>
+__global__ __launch_bounds__(256) void cache_kernel(const float* __restrict__ x,
+                                                    float* __restrict__ h,
+                                                    float* __restrict__ r, int64_t n) {
+  const int64_t n4 = n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const float4* x4 = reinterpret_cast<const float4*>(x);
+  float4* h4 = reinterpret_cast<float4*>(h);
+  float4* r4 = reinterpret_cast<float4*>(r);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    float4 a = *(x4 + i);
+    if (OP == ACID_CACHE_STORE) {
+      float4 b = *(h4 + i);
+      *(r4 + i) = make_float4(b.x - a.x, b.y - a.y, b.z - a.z, b.w - a.w);
+    } else {
+      float4 b = *(r4 + i);
+      *(h4 + i) = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
+    int64_t i = n4 * 4 + threadIdx.x;
+    if (OP == ACID_CACHE_STORE)
+      r[i] = h[i] - x[i];
+    else
+      h[i] = x[i] + r[i];
+  }
+}
+
+// fp32 [in][out] -> [out][in] (dtype), 32x32 tiles through LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_convert_kernel(const float* __restrict__ src,
+                                                                int64_t nin, int64_t nout,
+                                                                T* __restrict__ dst) {
+  __shared__ float tile[32][33];
+  const int64_t o0 = (int64_t)blockIdx.x * 32, i0 = (int64_t)blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+  for (int k = ty; k < 32; k += 8) {
+    int64_t i = i0 + k, o = o0 + tx;
+    tile[k][tx] = (i < nin && o < nout) ? src[i * nout + o] : 0.f;
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    int64_t o = o0 + k, i = i0 + tx;
+    if (o < nout && i < nin) dst[o * nin + i] = (T)tile[tx][k];
+  }
+}
+
+}  // namespace
+
+#define ACID_ROW_DISPATCH(CPL_VAR, MACRO) \
+  switch (CPL_VAR) {                      \
+    case 1: MACRO(1); break;              \
+    case 2: MACRO(2); break;              \
+    case 3: MACRO(3); break;              \
+    case 4: MACRO(4); break;              \
+    case 5: MACRO(5); break;              \
+    case 6: MACRO(6); break;              \
+    case 8: MACRO(8); break;              \
+    case 12: MACRO(12); break;            \
+    case 16: MACRO(16); break;            \
+    default: return hipErrorInvalidValue; \
+  }
+
+static int row_chunks(int H) {
+  // float4 chunks per lane, rounded to a compiled instantiation
+  int c = (H / 4 + 63) / 64;
+  if (c <= 6) return c;
+  if (c <= 8) return 8;
+  if (c <= 12) return 12;
+  if (c <= 16) return 16;
+  return -1;
+}
+
+hipError_t launch_ln_modulate(int out_dtype, const float* x, int64_t rows, int H,
+                              const float* shift, const float* scale, void* out,
+                              hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  const int cpl = row_chunks(H);
+  dim3 grid((unsigned)((rows + kRowsPerBlock - 1) / kRowsPerBlock));
+#define LN_BF(C) hipLaunchKernelGGL((ln_modulate_kernel<C, bf16>), grid, dim3(256), 0, s, x, rows, H, shift, scale, (bf16*)out)
+#define LN_F(C) hipLaunchKernelGGL((ln_modulate_kernel<C, float>), grid, dim3(256), 0, s, x, rows, H, shift, scale, (float*)out)
+  if (out_dtype == ACID_BF16) {
+    ACID_ROW_DISPATCH(cpl, LN_BF)
+  } else {
+    ACID_ROW_DISPATCH(cpl, LN_F)
+  }
+#undef LN_BF
+#undef LN_F
+  return hipGetLastError();
+}
+
+hipError_t launch_temni_drift(const float* x, int64_t rows, int H, const float* shift,
+                              const float* scale, const float* m_prev, float* m_cur,
+                              double* partials, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  const int cpl = row_chunks(H);
+  dim3 grid((unsigned)((rows + kRowsPerBlock - 1) / kRowsPerBlock));
+#define TD(C) hipLaunchKernelGGL((temni_drift_kernel<C>), grid, dim3(256), 0, s, x, rows, H, shift, scale, m_prev, m_cur, partials)
+  ACID_ROW_DISPATCH(cpl, TD)
+#undef TD
+  return hipGetLastError();
+}
+
+hipError_t launch_drift_finalize(const double* partials, int64_t rows, double* out,
+                                 hipStream_t s) {
+  hipLaunchKernelGGL(drift_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, rows, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  int64_t n4 = (n + 3) / 4;
+  int64_t blocks = (n4 + 255) / 256;
+  if (blocks > 256 * 16) blocks = 256 * 16;
+  if (op == ACID_CACHE_STORE)
+    hipLaunchKernelGGL(cache_kernel<ACID_CACHE_STORE>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
+  else
+    hipLaunchKernelGGL(cache_kernel<ACID_CACHE_APPLY>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_convert(const float* src, int64_t nin, int64_t nout, int dtype,
+                                    void* dst, hipStream_t s) {
+  dim3 grid((unsigned)((nout + 31) / 32), (unsigned)((nin + 31) / 32));
+  if (dtype == ACID_BF16)
+    hipLaunchKernelGGL(transpose_convert_kernel<bf16>, grid, dim3(256), 0, s, src, nin, nout, (bf16*)dst);
+  else
+    hipLaunchKernelGGL(transpose_convert_kernel<float>, grid, dim3(256), 0, s, src, nin, nout, (float*)dst);
+  return hipGetLastError();
+}
+
+}  // namespace acid

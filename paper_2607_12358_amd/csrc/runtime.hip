@@ -1,0 +1,734 @@
+// Host runtime of libacid: configuration checks, the weight-arena and
+// workspace layouts, the DiT step, the drift signal, the residual cache and
+// the ACID-gated denoise loop.  All device memory is the caller's; this file
+// only carves it up and launches kernels on the caller's stream.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "common.h"
+
+#define ACID_VERSION "0.1.0"
+
+namespace acid {
+
+static thread_local char g_err[512] = "";
+
+acid_status set_error(acid_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+acid_status check_hip(hipError_t e, const char* what) {
+  return set_error(ACID_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t a) { return (a + kAlign - 1) / kAlign * kAlign; }
+
+int esize(int dtype) { return dtype == ACID_BF16 ? 2 : 4; }
+
+acid_status check_config(const acid_dit_config* c) {
+  if (!c) return set_error(ACID_ERR_INVALID_ARG, "config is NULL");
+  if (c->dtype != ACID_F32 && c->dtype != ACID_BF16)
+    return set_error(ACID_ERR_INVALID_ARG, "dtype %d is not ACID_F32 or ACID_BF16", c->dtype);
+  if (c->n_blocks < 1 || c->n_video < 1 || c->n_text < 0 || c->n_heads < 1)
+    return set_error(ACID_ERR_INVALID_ARG, "n_blocks, n_video, n_heads must be >= 1 and n_text >= 0");
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return set_error(ACID_ERR_SHAPE, "head_dim %d: supported 64 or 128", c->head_dim);
+  if ((int64_t)c->n_heads * c->head_dim != c->hidden)
+    return set_error(ACID_ERR_SHAPE, "hidden %d != n_heads %d * head_dim %d", c->hidden, c->n_heads,
+                     c->head_dim);
+  if (c->hidden % 128 || c->hidden > 4096)
+    return set_error(ACID_ERR_SHAPE, "hidden %d: must be a multiple of 128 and <= 4096", c->hidden);
+  if (c->ffn < 128 || c->ffn % 128)
+    return set_error(ACID_ERR_SHAPE, "ffn %d: must be a positive multiple of 128", c->ffn);
+  if (c->freq_dim < 2 || c->freq_dim % 2 || c->freq_dim > 1024)
+    return set_error(ACID_ERR_SHAPE, "freq_dim %d: must be even and <= 1024", c->freq_dim);
+  return ACID_OK;
+}
+
+// ------------------------------------------------------------ arena layout
+struct WeightLayout {
+  size_t temb_w1, temb_b1, temb_w2, temb_b2;
+  size_t blk0;        // offset of block 0
+  size_t blk_stride;  // bytes between consecutive blocks
+  // offsets within a block
+  size_t ada_w, ada_b, qkv_w, qkv_b, o_w, o_b, f1_w, f1_b, f2_w, f2_b;
+  size_t head_ada_w, head_ada_b, head_w, head_b;
+  size_t total;
+};
+
+WeightLayout weight_layout(const acid_dit_config& c) {
+  WeightLayout L;
+  const size_t H = c.hidden, F = c.ffn, Ft = c.freq_dim, es = esize(c.dtype);
+  size_t off = 0;
+  auto put = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.temb_w1 = put(Ft * H * 4);
+  L.temb_b1 = put(H * 4);
+  L.temb_w2 = put(H * H * 4);
+  L.temb_b2 = put(H * 4);
+  L.blk0 = off;
+  size_t b = 0;
+  auto putb = [&](size_t bytes) {
+    size_t o = b;
+    b = align_up(b + bytes);
+    return o;
+  };
+  L.ada_w = putb(H * 6 * H * 4);
+  L.ada_b = putb(6 * H * 4);
+  L.qkv_w = putb(3 * H * H * es);
+  L.qkv_b = putb(3 * H * 4);
+  L.o_w = putb(H * H * es);
+  L.o_b = putb(H * 4);
+  L.f1_w = putb(F * H * es);
+  L.f1_b = putb(F * 4);
+  L.f2_w = putb(H * F * es);
+  L.f2_b = putb(H * 4);
+  L.blk_stride = b;
+  off += b * c.n_blocks;
+  L.head_ada_w = put(H * 2 * H * 4);
+  L.head_ada_b = put(2 * H * 4);
+  L.head_w = put(H * H * es);
+  L.head_b = put(H * 4);
+  L.total = off;
+  return L;
+}
+
+struct WorkLayout {
+  size_t h, act, q, k, vt, o, g, modtab, temb_e, temb_hid, temb_u, partials, dres, m0, m1, r, v;
+  size_t total;
+  int64_t vt_ld;
+};
+
+WorkLayout work_layout(const acid_dit_config& c, int max_steps) {
+  WorkLayout W;
+  const size_t H = c.hidden, F = c.ffn, Ft = c.freq_dim, es = esize(c.dtype);
+  const size_t Lv = c.n_video, L = (size_t)c.n_text + c.n_video;
+  const size_t S = max_steps < 1 ? 1 : max_steps;
+  W.vt_ld = round_up((int64_t)L, 8);
+  size_t off = 0;
+  auto put = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  W.h = put(L * H * 4);
+  W.act = put(L * H * es);
+  W.q = put(L * H * es);
+  W.k = put(L * H * es);
+  W.vt = put((size_t)c.n_heads * c.head_dim * W.vt_ld * es);
+  W.o = put(L * H * es);
+  W.g = put(L * F * es);
+  W.modtab = put(S * (6 * (size_t)c.n_blocks + 2) * H * 4);
+  W.temb_e = put(S * Ft * 4);
+  W.temb_hid = put(S * H * 4);
+  W.temb_u = put(S * H * 4);
+  W.partials = put(Lv * 2 * sizeof(double));
+  W.dres = put(4 * sizeof(double));
+  W.m0 = put(Lv * H * 4);
+  W.m1 = put(Lv * H * 4);
+  W.r = put(Lv * H * 4);
+  W.v = put(Lv * H * 4);
+  W.total = off;
+  return W;
+}
+
+}  // namespace
+}  // namespace acid
+
+using namespace acid;
+
+struct acid_model {
+  acid_dit_config cfg;
+  int max_steps;
+  char* wb;  // weight arena
+  char* ws;  // workspace
+  WeightLayout wl;
+  WorkLayout kl;
+  // timing
+  bool timing = false;
+  struct Pending {
+    int cls;
+    hipEvent_t e0, e1;
+  };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> pool;
+  double total_ms[ACID_K_COUNT] = {};
+  int64_t launches[ACID_K_COUNT] = {};
+
+  int H() const { return cfg.hidden; }
+  int64_t Lv() const { return cfg.n_video; }
+  int64_t Lt() const { return cfg.n_text; }
+  int64_t L() const { return (int64_t)cfg.n_text + cfg.n_video; }
+  int64_t rowsz() const { return (6 * (int64_t)cfg.n_blocks + 2) * cfg.hidden; }
+  template <class T = float>
+  T* wp(size_t off) const { return reinterpret_cast<T*>(wb + off); }
+  template <class T = float>
+  T* bp(int b, size_t off) const { return reinterpret_cast<T*>(wb + wl.blk0 + (size_t)b * wl.blk_stride + off); }
+  template <class T = float>
+  T* kp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+};
+
+namespace {
+
+acid_status harvest(acid_model* m) {
+  for (auto& p : m->pending) {
+    ACID_HIP(hipEventSynchronize(p.e1));
+    float ms = 0.f;
+    ACID_HIP(hipEventElapsedTime(&ms, p.e0, p.e1));
+    m->total_ms[p.cls] += ms;
+    m->launches[p.cls] += 1;
+    m->pool.push_back(p.e0);
+    m->pool.push_back(p.e1);
+  }
+  m->pending.clear();
+  return ACID_OK;
+}
+
+acid_status get_event(acid_model* m, hipEvent_t* e) {
+  if (m->pool.empty()) {
+    ACID_HIP(hipEventCreate(e));
+  } else {
+    *e = m->pool.back();
+    m->pool.pop_back();
+  }
+  return ACID_OK;
+}
+
+// Launches f() on stream s, bracketed by timing events when enabled.
+template <class F>
+acid_status run(acid_model* m, int cls, hipStream_t s, const char* what, F&& f) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (m->timing) {
+    if (m->pending.size() > 4096) ACID_TRY(harvest(m));
+    ACID_TRY(get_event(m, &e0));
+    ACID_TRY(get_event(m, &e1));
+    ACID_HIP(hipEventRecord(e0, s));
+  }
+  hipError_t err = f();
+  if (err != hipSuccess) return check_hip(err, what);
+  if (m->timing) {
+    ACID_HIP(hipEventRecord(e1, s));
+    m->pending.push_back({cls, e0, e1});
+  }
+  return ACID_OK;
+}
+
+// ------------------------------------------------------------ model pieces
+
+acid_status modulation_table(acid_model* m, const float* sigmas, int n, float* table,
+                             hipStream_t s) {
+  const acid_dit_config& c = m->cfg;
+  const int H = c.hidden, Ft = c.freq_dim;
+  float* e = m->kp(m->kl.temb_e);
+  float* hid = m->kp(m->kl.temb_hid);
+  float* u = m->kp(m->kl.temb_u);
+  const int64_t bstride = (int64_t)(m->wl.blk_stride / 4);
+  return run(m, ACID_K_TEMB, s, "timestep modulation", [&]() {
+    hipError_t err = launch_sinusoid(sigmas, n, Ft, e, s);
+    if (err == hipSuccess)
+      err = launch_skinny_gemm(e, Ft, n, Ft, m->wp(m->wl.temb_w1), H, m->wp(m->wl.temb_b1), hid,
+                               H, 1, 1, 0, 0, 0, s);
+    if (err == hipSuccess)
+      err = launch_skinny_gemm(hid, H, n, H, m->wp(m->wl.temb_w2), H, m->wp(m->wl.temb_b2), u, H,
+                               1, 1, 0, 0, 0, s);
+    if (err == hipSuccess)
+      err = launch_skinny_gemm(u, H, n, H, m->bp(0, m->wl.ada_w), 6 * H, m->bp(0, m->wl.ada_b),
+                               table, m->rowsz(), 0, c.n_blocks, bstride, bstride,
+                               6 * (int64_t)H, s);
+    if (err == hipSuccess)
+      err = launch_skinny_gemm(u, H, n, H, m->wp(m->wl.head_ada_w), 2 * H,
+                               m->wp(m->wl.head_ada_b), table + 6 * (int64_t)c.n_blocks * H,
+                               m->rowsz(), 0, 1, 0, 0, 0, s);
+    return err;
+  });
+}
+
+acid_status ln_mod(acid_model* m, const float* x, int64_t rows, const float* shift,
+                   const float* scale, void* out, hipStream_t s) {
+  return run(m, ACID_K_LN_MOD, s, "ln_modulate", [&]() {
+    return launch_ln_modulate(m->cfg.dtype, x, rows, m->H(), shift, scale, out, s);
+  });
+}
+
+acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hipStream_t s) {
+  const acid_dit_config& c = m->cfg;
+  const int H = c.hidden, F = c.ffn;
+  const int64_t L = m->L();
+  void* act = m->kp<void>(m->kl.act);
+  void* o = m->kp<void>(m->kl.o);
+  void* g = m->kp<void>(m->kl.g);
+  const int dt = c.dtype;
+
+  ACID_TRY(ln_mod(m, h, L, mod6, mod6 + H, act, s));
+
+  acid_epilogue_args e = {};
+  e.kind = ACID_EPI_QKV;
+  e.bias = m->bp(b, m->wl.qkv_b);
+  e.q = m->kp<void>(m->kl.q);
+  e.k = m->kp<void>(m->kl.k);
+  e.vt = m->kp<void>(m->kl.vt);
+  e.vt_ld = m->kl.vt_ld;
+  e.n_heads = c.n_heads;
+  e.head_dim = c.head_dim;
+  ACID_TRY(run(m, ACID_K_GEMM_QKV, s, "qkv gemm", [&]() {
+    return launch_linear(dt, L, 3 * H, H, act, m->bp<void>(b, m->wl.qkv_w), e, s);
+  }));
+  ACID_TRY(run(m, ACID_K_ATTENTION, s, "attention", [&]() {
+    return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, o, s);
+  }));
+  acid_epilogue_args p = {};
+  p.kind = ACID_EPI_GATE_RESIDUAL;
+  p.bias = m->bp(b, m->wl.o_b);
+  p.gate = mod6 + 2 * H;
+  p.out = h;
+  ACID_TRY(run(m, ACID_K_GEMM_PROJ, s, "proj gemm", [&]() {
+    return launch_linear(dt, L, H, H, o, m->bp<void>(b, m->wl.o_w), p, s);
+  }));
+  ACID_TRY(ln_mod(m, h, L, mod6 + 3 * H, mod6 + 4 * H, act, s));
+  acid_epilogue_args f1 = {};
+  f1.kind = ACID_EPI_BIAS_GELU;
+  f1.bias = m->bp(b, m->wl.f1_b);
+  f1.out = g;
+  ACID_TRY(run(m, ACID_K_GEMM_FFN1, s, "ffn1 gemm", [&]() {
+    return launch_linear(dt, L, F, H, act, m->bp<void>(b, m->wl.f1_w), f1, s);
+  }));
+  acid_epilogue_args f2 = {};
+  f2.kind = ACID_EPI_GATE_RESIDUAL;
+  f2.bias = m->bp(b, m->wl.f2_b);
+  f2.gate = mod6 + 5 * H;
+  f2.out = h;
+  ACID_TRY(run(m, ACID_K_GEMM_FFN2, s, "ffn2 gemm", [&]() {
+    return launch_linear(dt, L, H, F, g, m->bp<void>(b, m->wl.f2_w), f2, s);
+  }));
+  return ACID_OK;
+}
+
+// h = [text; x], all blocks with the modulation row `row`.
+acid_status stack_forward(acid_model* m, const float* row, const float* x, const float* text,
+                          hipStream_t s) {
+  const int H = m->H();
+  float* h = m->kp(m->kl.h);
+  ACID_TRY(run(m, ACID_K_MISC, s, "assemble residual stream", [&]() {
+    hipError_t err = hipSuccess;
+    if (m->Lt() > 0)
+      err = hipMemcpyAsync(h, text, (size_t)m->Lt() * H * 4, hipMemcpyDeviceToDevice, s);
+    if (err == hipSuccess)
+      err = hipMemcpyAsync(h + m->Lt() * H, x, (size_t)m->Lv() * H * 4, hipMemcpyDeviceToDevice,
+                           s);
+    return err;
+  }));
+  for (int b = 0; b < m->cfg.n_blocks; ++b)
+    ACID_TRY(block_forward(m, b, row + 6 * (int64_t)b * H, h, s));
+  return ACID_OK;
+}
+
+// v = LN-modulated head of h_v; EULER variant updates x in place.
+acid_status head_forward(acid_model* m, const float* row, const float* hv, float* v_out,
+                         float* x_euler, float dsigma, hipStream_t s) {
+  const acid_dit_config& c = m->cfg;
+  const int H = c.hidden;
+  const float* shift = row + 6 * (int64_t)c.n_blocks * H;
+  void* act = m->kp<void>(m->kl.act);
+  ACID_TRY(ln_mod(m, hv, m->Lv(), shift, shift + H, act, s));
+  acid_epilogue_args e = {};
+  e.bias = m->wp(m->wl.head_b);
+  if (x_euler) {
+    e.kind = ACID_EPI_EULER;
+    e.out = x_euler;
+    e.v_out = v_out;
+    e.dsigma = dsigma;
+  } else {
+    e.kind = ACID_EPI_BIAS;
+    e.out = v_out;
+  }
+  return run(m, ACID_K_GEMM_HEAD, s, "head gemm", [&]() {
+    return launch_linear(c.dtype, m->Lv(), H, H, act, m->wp<void>(m->wl.head_w), e, s);
+  });
+}
+
+// TEMNI into m_cur; if m_prev, the relative-L1 drift is reduced into dres.
+acid_status drift(acid_model* m, const float* row, const float* x, const float* m_prev,
+                  float* m_cur, hipStream_t s) {
+  const int H = m->H();
+  double* part = m->kp<double>(m->kl.partials);
+  double* dres = m->kp<double>(m->kl.dres);
+  return run(m, ACID_K_DRIFT, s, "drift", [&]() {
+    hipError_t err = launch_temni_drift(x, m->Lv(), H, row, row + H, m_prev, m_cur, part, s);
+    if (err == hipSuccess && m_prev) err = launch_drift_finalize(part, m->Lv(), dres, s);
+    return err;
+  });
+}
+
+acid_status read_drift(acid_model* m, double* s_out, hipStream_t s) {
+  double res[3];
+  ACID_HIP(hipMemcpyAsync(res, m->kp<double>(m->kl.dres), sizeof res, hipMemcpyDeviceToHost, s));
+  ACID_HIP(hipStreamSynchronize(s));
+  *s_out = res[2];
+  return ACID_OK;
+}
+
+}  // namespace
+
+// ====================================================================== ABI
+
+extern "C" {
+
+const char* acid_version(void) { return ACID_VERSION " (gfx950)"; }
+
+const char* acid_last_error(void) { return g_err; }
+
+acid_status acid_config_check(const acid_dit_config* cfg) { return check_config(cfg); }
+
+size_t acid_weights_bytes(const acid_dit_config* cfg) {
+  if (check_config(cfg) != ACID_OK) return 0;
+  return weight_layout(*cfg).total;
+}
+
+size_t acid_workspace_bytes(const acid_dit_config* cfg, int32_t max_steps) {
+  if (check_config(cfg) != ACID_OK || max_steps < 1) return 0;
+  return work_layout(*cfg, max_steps).total;
+}
+
+int32_t acid_tensor_count(const acid_dit_config* cfg) {
+  if (check_config(cfg) != ACID_OK) return 0;
+  return 8 + 10 * cfg->n_blocks;
+}
+
+namespace {
+// kind: 0 fp32 copy, 1 GEMM weight (transpose + convert)
+struct TensorInfo {
+  int rank;
+  int64_t d0, d1;
+  int gemm;
+  size_t off;  // absolute offset in the arena
+};
+
+acid_status tensor_info(const acid_dit_config& c, int id, TensorInfo* t) {
+  const int64_t H = c.hidden, F = c.ffn, Ft = c.freq_dim;
+  const int nb = c.n_blocks;
+  const WeightLayout L = weight_layout(c);
+  if (id < 0 || id >= 8 + 10 * nb) return set_error(ACID_ERR_INVALID_ARG, "tensor id %d out of range", id);
+  auto set = [&](int rank, int64_t d0, int64_t d1, int gemm, size_t off) {
+    *t = TensorInfo{rank, d0, d1, gemm, off};
+    return ACID_OK;
+  };
+  if (id < 4) {
+    switch (id) {
+      case 0: return set(2, Ft, H, 0, L.temb_w1);
+      case 1: return set(1, H, 1, 0, L.temb_b1);
+      case 2: return set(2, H, H, 0, L.temb_w2);
+      default: return set(1, H, 1, 0, L.temb_b2);
+    }
+  }
+  if (id < 4 + 10 * nb) {
+    const int b = (id - 4) / 10, j = (id - 4) % 10;
+    const size_t base = L.blk0 + (size_t)b * L.blk_stride;
+    switch (j) {
+      case 0: return set(2, H, 6 * H, 0, base + L.ada_w);
+      case 1: return set(1, 6 * H, 1, 0, base + L.ada_b);
+      case 2: return set(2, H, 3 * H, 1, base + L.qkv_w);
+      case 3: return set(1, 3 * H, 1, 0, base + L.qkv_b);
+      case 4: return set(2, H, H, 1, base + L.o_w);
+      case 5: return set(1, H, 1, 0, base + L.o_b);
+      case 6: return set(2, H, F, 1, base + L.f1_w);
+      case 7: return set(1, F, 1, 0, base + L.f1_b);
+      case 8: return set(2, F, H, 1, base + L.f2_w);
+      default: return set(1, H, 1, 0, base + L.f2_b);
+    }
+  }
+  switch (id - 4 - 10 * nb) {
+    case 0: return set(2, H, 2 * H, 0, L.head_ada_w);
+    case 1: return set(1, 2 * H, 1, 0, L.head_ada_b);
+    case 2: return set(2, H, H, 1, L.head_w);
+    default: return set(1, H, 1, 0, L.head_b);
+  }
+}
+}  // namespace
+
+acid_status acid_tensor_shape(const acid_dit_config* cfg, int32_t id, int32_t* rank,
+                              int64_t dims[2]) {
+  ACID_TRY(check_config(cfg));
+  if (!rank || !dims) return set_error(ACID_ERR_INVALID_ARG, "rank/dims is NULL");
+  TensorInfo t;
+  ACID_TRY(tensor_info(*cfg, id, &t));
+  *rank = t.rank;
+  dims[0] = t.d0;
+  dims[1] = t.rank == 2 ? t.d1 : 1;
+  return ACID_OK;
+}
+
+acid_status acid_model_create(const acid_dit_config* cfg, void* weights_dev, void* workspace_dev,
+                              int32_t max_steps, acid_model** out) {
+  ACID_TRY(check_config(cfg));
+  if (!weights_dev || !workspace_dev || !out)
+    return set_error(ACID_ERR_INVALID_ARG, "weights, workspace and out must be non-NULL");
+  if (max_steps < 1) return set_error(ACID_ERR_INVALID_ARG, "max_steps %d < 1", max_steps);
+  if (((uintptr_t)weights_dev | (uintptr_t)workspace_dev) % 256)
+    return set_error(ACID_ERR_INVALID_ARG, "weights and workspace must be 256-byte aligned");
+  acid_model* m = new (std::nothrow) acid_model();
+  if (!m) return set_error(ACID_ERR_INVALID_ARG, "host allocation failed");
+  m->cfg = *cfg;
+  m->max_steps = max_steps;
+  m->wb = static_cast<char*>(weights_dev);
+  m->ws = static_cast<char*>(workspace_dev);
+  m->wl = weight_layout(*cfg);
+  m->kl = work_layout(*cfg, max_steps);
+  *out = m;
+  return ACID_OK;
+}
+
+acid_status acid_model_load_tensor(acid_model* m, int32_t id, const float* src_dev, int64_t n,
+                                   hipStream_t stream) {
+  if (!m || !src_dev) return set_error(ACID_ERR_INVALID_ARG, "model and source must be non-NULL");
+  TensorInfo t;
+  ACID_TRY(tensor_info(m->cfg, id, &t));
+  const int64_t count = t.rank == 2 ? t.d0 * t.d1 : t.d0;
+  if (n != count)
+    return set_error(ACID_ERR_SHAPE, "tensor %d has %lld elements, got %lld", id, (long long)count,
+                     (long long)n);
+  void* dst = m->wb + t.off;
+  return run(m, ACID_K_MISC, stream, "load tensor", [&]() {
+    if (t.gemm) return launch_transpose_convert(src_dev, t.d0, t.d1, m->cfg.dtype, dst, stream);
+    return hipMemcpyAsync(dst, src_dev, (size_t)count * 4, hipMemcpyDeviceToDevice, stream);
+  });
+}
+
+void acid_model_destroy(acid_model* m) {
+  if (!m) return;
+  harvest(m);
+  for (auto e : m->pool) hipEventDestroy(e);
+  delete m;
+}
+
+acid_status acid_model_set_timing(acid_model* m, int32_t enable) {
+  if (!m) return set_error(ACID_ERR_INVALID_ARG, "model is NULL");
+  if (!enable) ACID_TRY(harvest(m));
+  m->timing = enable != 0;
+  return ACID_OK;
+}
+
+acid_status acid_model_reset_timing(acid_model* m) {
+  if (!m) return set_error(ACID_ERR_INVALID_ARG, "model is NULL");
+  ACID_TRY(harvest(m));
+  for (int i = 0; i < ACID_K_COUNT; ++i) {
+    m->total_ms[i] = 0;
+    m->launches[i] = 0;
+  }
+  return ACID_OK;
+}
+
+acid_status acid_model_timing(acid_model* m, int32_t cls, double* total_ms, int64_t* launches) {
+  if (!m || !total_ms || !launches) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (cls < 0 || cls >= ACID_K_COUNT) return set_error(ACID_ERR_INVALID_ARG, "kernel class %d", cls);
+  ACID_TRY(harvest(m));
+  *total_ms = m->total_ms[cls];
+  *launches = m->launches[cls];
+  return ACID_OK;
+}
+
+acid_status acid_timestep_modulation(acid_model* m, const float* sigmas_host, int32_t n,
+                                     float* table_dev, hipStream_t stream) {
+  if (!m || !sigmas_host || !table_dev) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (n < 1 || n > m->max_steps)
+    return set_error(ACID_ERR_INVALID_ARG, "n %d must be in [1, max_steps=%d]", n, m->max_steps);
+  return modulation_table(m, sigmas_host, n, table_dev, stream);
+}
+
+acid_status acid_ln_modulate(int32_t out_dtype, const float* x_dev, int64_t rows, int32_t hidden,
+                             const float* shift_dev, const float* scale_dev, void* out_dev,
+                             hipStream_t stream) {
+  if (out_dtype != ACID_F32 && out_dtype != ACID_BF16)
+    return set_error(ACID_ERR_INVALID_ARG, "bad dtype %d", out_dtype);
+  if (rows < 0) return set_error(ACID_ERR_INVALID_ARG, "rows < 0");
+  if (hidden < 4 || hidden % 4 || hidden > 4096)
+    return set_error(ACID_ERR_SHAPE, "hidden %d: multiple of 4 in [4, 4096]", hidden);
+  if (rows > 0 && (!x_dev || !shift_dev || !scale_dev || !out_dev))
+    return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  hipError_t e = launch_ln_modulate(out_dtype, x_dev, rows, hidden, shift_dev, scale_dev, out_dev,
+                                    stream);
+  return e == hipSuccess ? ACID_OK : check_hip(e, "ln_modulate");
+}
+
+acid_status acid_attention(int32_t dtype, int32_t n_heads, int64_t seq_len, int32_t head_dim,
+                           const void* q_dev, const void* k_dev, const void* vt_dev,
+                           int64_t vt_ld, void* o_dev, hipStream_t stream) {
+  if (dtype != ACID_F32 && dtype != ACID_BF16)
+    return set_error(ACID_ERR_INVALID_ARG, "bad dtype %d", dtype);
+  if (n_heads < 1 || seq_len < 0) return set_error(ACID_ERR_INVALID_ARG, "n_heads < 1 or seq_len < 0");
+  if (head_dim != 64 && head_dim != 128)
+    return set_error(ACID_ERR_SHAPE, "head_dim %d: supported 64 or 128", head_dim);
+  if (vt_ld < round_up(seq_len, 8) || vt_ld % 8)
+    return set_error(ACID_ERR_SHAPE, "vt_ld %lld must be a multiple of 8 and >= round_up(L, 8)",
+                     (long long)vt_ld);
+  if (seq_len > 0 && (!q_dev || !k_dev || !vt_dev || !o_dev))
+    return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  hipError_t e = launch_attention(dtype, n_heads, seq_len, head_dim, q_dev, k_dev, vt_dev, vt_ld,
+                                  o_dev, stream);
+  return e == hipSuccess ? ACID_OK : check_hip(e, "attention");
+}
+
+acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K, const void* a_dev,
+                        const void* wt_dev, const acid_epilogue_args* epi, hipStream_t stream) {
+  if (dtype != ACID_F32 && dtype != ACID_BF16)
+    return set_error(ACID_ERR_INVALID_ARG, "bad dtype %d", dtype);
+  if (!epi) return set_error(ACID_ERR_INVALID_ARG, "epilogue args NULL");
+  if (M < 0 || N <= 0 || K <= 0) return set_error(ACID_ERR_INVALID_ARG, "bad M/N/K");
+  if (N % 128 || K % 64)
+    return set_error(ACID_ERR_SHAPE, "N %d must be a multiple of 128 and K %d of 64", N, K);
+  if (M == 0) return ACID_OK;
+  if (!a_dev || !wt_dev || !epi->bias) return set_error(ACID_ERR_INVALID_ARG, "NULL operand or bias");
+  switch (epi->kind) {
+    case ACID_EPI_BIAS:
+    case ACID_EPI_BIAS_GELU:
+    case ACID_EPI_EULER:
+      if (!epi->out) return set_error(ACID_ERR_INVALID_ARG, "out is NULL");
+      break;
+    case ACID_EPI_GATE_RESIDUAL:
+      if (!epi->out || !epi->gate) return set_error(ACID_ERR_INVALID_ARG, "out/gate NULL");
+      break;
+    case ACID_EPI_QKV:
+      if (!epi->q || !epi->k || !epi->vt) return set_error(ACID_ERR_INVALID_ARG, "q/k/vt NULL");
+      if (epi->head_dim < 1 || epi->n_heads < 1 ||
+          (int64_t)3 * epi->n_heads * epi->head_dim != N || epi->head_dim % 32)
+        return set_error(ACID_ERR_SHAPE, "QKV: N must be 3 * n_heads * head_dim, head_dim % 32 == 0");
+      if (epi->vt_ld < M) return set_error(ACID_ERR_SHAPE, "QKV: vt_ld < M");
+      break;
+    default: return set_error(ACID_ERR_INVALID_ARG, "bad epilogue kind %d", epi->kind);
+  }
+  hipError_t e = launch_linear(dtype, M, N, K, a_dev, wt_dev, *epi, stream);
+  return e == hipSuccess ? ACID_OK : check_hip(e, "linear");
+}
+
+acid_status acid_block_forward(acid_model* m, int32_t block, const float* mod6_dev, float* h_dev,
+                               hipStream_t stream) {
+  if (!m || !mod6_dev || !h_dev) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (block < 0 || block >= m->cfg.n_blocks)
+    return set_error(ACID_ERR_INVALID_ARG, "block %d out of range", block);
+  return block_forward(m, block, mod6_dev, h_dev, stream);
+}
+
+acid_status acid_cache_apply(acid_cache_op op, const float* x_dev, float* h_out_dev, float* r_dev,
+                             int64_t n, hipStream_t stream) {
+  if (op != ACID_CACHE_STORE && op != ACID_CACHE_APPLY)
+    return set_error(ACID_ERR_INVALID_ARG, "bad cache op %d", (int)op);
+  if (n < 0) return set_error(ACID_ERR_INVALID_ARG, "n < 0");
+  if (n == 0) return ACID_OK;
+  if (!x_dev || !h_out_dev || !r_dev) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (((uintptr_t)x_dev | (uintptr_t)h_out_dev | (uintptr_t)r_dev) % 16)
+    return set_error(ACID_ERR_INVALID_ARG, "cache buffers must be 16-byte aligned");
+  hipError_t e = launch_cache(op, x_dev, h_out_dev, r_dev, n, stream);
+  return e == hipSuccess ? ACID_OK : check_hip(e, "cache");
+}
+
+acid_status acid_dit_step(acid_model* m, const float* x_dev, float sigma, const float* text_dev,
+                          float* v_dev, float* resid_dev, hipStream_t stream) {
+  if (!m || !x_dev || !v_dev) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if ((m->cfg.n_text > 0) != (text_dev != nullptr))
+    return set_error(ACID_ERR_INVALID_ARG, "text must be given iff n_text > 0");
+  float* row = m->kp(m->kl.modtab);
+  ACID_TRY(modulation_table(m, &sigma, 1, row, stream));
+  ACID_TRY(stack_forward(m, row, x_dev, text_dev, stream));
+  float* hv = m->kp(m->kl.h) + m->Lt() * m->H();
+  if (resid_dev) {
+    ACID_TRY(run(m, ACID_K_CACHE, stream, "cache store", [&]() {
+      return launch_cache(ACID_CACHE_STORE, x_dev, hv, resid_dev, m->Lv() * m->H(), stream);
+    }));
+  }
+  return head_forward(m, row, hv, v_dev, nullptr, 0.f, stream);
+}
+
+acid_status acid_drift_signal(acid_model* m, const float* x_dev, float sigma,
+                              const float* m_prev_dev, float* m_cur_dev, double* s_out,
+                              hipStream_t stream) {
+  if (!m || !x_dev || !m_cur_dev || !s_out) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  float* row = m->kp(m->kl.modtab);
+  ACID_TRY(modulation_table(m, &sigma, 1, row, stream));
+  ACID_TRY(drift(m, row, x_dev, m_prev_dev, m_cur_dev, stream));
+  if (!m_prev_dev) {
+    ACID_HIP(hipStreamSynchronize(stream));
+    *s_out = NAN;
+    return ACID_OK;
+  }
+  return read_drift(m, s_out, stream);
+}
+
+acid_status acid_denoise_loop(acid_model* m, float* x_dev, const float* sigmas_host,
+                              int32_t n_steps, const float* text_dev, int32_t mode,
+                              const acid_gate_params* gate, const uint8_t* forced,
+                              acid_step_trace* trace, hipStream_t stream) {
+  if (!m || !x_dev || !sigmas_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID)
+    return set_error(ACID_ERR_INVALID_ARG, "bad mode %d", mode);
+  if (mode == ACID_MODE_ACID && !gate) return set_error(ACID_ERR_INVALID_ARG, "gate params NULL");
+  if (n_steps < 1 || n_steps > m->max_steps)
+    return set_error(ACID_ERR_INVALID_ARG, "n_steps %d must be in [1, max_steps=%d]", n_steps,
+                     m->max_steps);
+  if ((m->cfg.n_text > 0) != (text_dev != nullptr))
+    return set_error(ACID_ERR_INVALID_ARG, "text must be given iff n_text > 0");
+  if (forced && !forced[0])
+    return set_error(ACID_ERR_INVALID_ARG, "forced schedule must compute step 0");
+  if (forced && mode == ACID_MODE_NOCACHE)
+    return set_error(ACID_ERR_UNSUPPORTED, "a forced schedule needs ACID mode (the residual cache)");
+
+  const int H = m->H();
+  const int64_t nv = m->Lv() * H;
+  float* table = m->kp(m->kl.modtab);
+  float* mbuf[2] = {m->kp(m->kl.m0), m->kp(m->kl.m1)};
+  float* r = m->kp(m->kl.r);
+  float* hv = m->kp(m->kl.h) + m->Lt() * H;
+  ACID_TRY(modulation_table(m, sigmas_host, n_steps, table, stream));
+
+  acid_gate_state st = {};
+  int cur = 0;
+  for (int i = 0; i < n_steps; ++i) {
+    const float* row = table + (int64_t)i * m->rowsz();
+    double s = NAN, tau = NAN;
+    int32_t gate_compute = 1;
+    if (mode == ACID_MODE_ACID) {
+      const float* mprev = i > 0 ? mbuf[cur ^ 1] : nullptr;
+      ACID_TRY(drift(m, row, x_dev, mprev, mbuf[cur], stream));
+      if (mprev) ACID_TRY(read_drift(m, &s, stream));
+      cur ^= 1;
+      ACID_TRY(acid_gate(&st, gate, s, &gate_compute, &tau));
+    }
+    const int compute = forced ? (forced[i] != 0) : gate_compute;
+    if (compute) {
+      ACID_TRY(stack_forward(m, row, x_dev, text_dev, stream));
+      if (mode == ACID_MODE_ACID) {
+        ACID_TRY(run(m, ACID_K_CACHE, stream, "cache store", [&]() {
+          return launch_cache(ACID_CACHE_STORE, x_dev, hv, r, nv, stream);
+        }));
+      }
+    } else {
+      ACID_TRY(run(m, ACID_K_CACHE, stream, "cache apply", [&]() {
+        return launch_cache(ACID_CACHE_APPLY, x_dev, hv, r, nv, stream);
+      }));
+    }
+    const float dsig = sigmas_host[i + 1] - sigmas_host[i];
+    ACID_TRY(head_forward(m, row, hv, nullptr, x_dev, dsig, stream));
+    if (trace) {
+      trace[i].compute = compute;
+      trace[i].gate_compute = gate_compute;
+      trace[i].s = s;
+      trace[i].sigma_sum_after = st.sigma_sum;
+      trace[i].tau_used = tau;
+    }
+  }
+  return ACID_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+"""The C-ABI library on the host (no GPU needed): it loads, exports every
+symbol include/acid.h declares, and its pure host logic (configuration
+checks, manifest shapes, sizes, the gate) behaves as specified."""
+import ctypes as C
+import math
+
+import numpy as np
+import pytest
+
+import acid_inputs as ai
+import oracle as O
+from paper_2607_12358_amd import _lib as L
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = L.header_symbols()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(lib, n), n
+    for n in ("acid_dit_step", "acid_drift_signal", "acid_gate", "acid_cache_apply",
+              "acid_denoise_loop"):
+        assert n in names
+
+
+def test_version(lib):
+    assert b"gfx950" in lib.acid_version()
+
+
+@pytest.mark.parametrize("cfg", list(ai.CONFIGS.values()), ids=list(ai.CONFIGS))
+def test_workload_configs_accepted_and_manifest_matches(lib, cfg):
+    c = L.config_c(cfg)
+    assert lib.acid_config_check(C.byref(c)) == 0, L.last_error()
+    man = ai.manifest(cfg)
+    assert lib.acid_tensor_count(C.byref(c)) == len(man)
+    for tid, (name, shape) in enumerate(man):
+        rank = C.c_int32()
+        dims = (C.c_int64 * 2)()
+        assert lib.acid_tensor_shape(C.byref(c), tid, C.byref(rank), dims) == 0
+        assert tuple(dims[:rank.value]) == shape, name
+    wb = lib.acid_weights_bytes(C.byref(c))
+    nparam = sum(int(np.prod(s)) for _, s in man)
+    assert nparam * 2 <= wb <= nparam * 4 + 256 * len(man)
+    assert lib.acid_workspace_bytes(C.byref(c), cfg.n_steps) > cfg.n_tokens * cfg.hidden * 4
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, L.ACID_ERR_SHAPE), ("hidden", 1000, L.ACID_ERR_SHAPE),
+    ("ffn", 1000, L.ACID_ERR_SHAPE), ("n_blocks", 0, L.ACID_ERR_INVALID_ARG),
+    ("freq_dim", 7, L.ACID_ERR_SHAPE), ("dtype", 5, L.ACID_ERR_INVALID_ARG)])
+def test_config_errors(lib, field, value, status):
+    c = L.config_c(ai.TINY)
+    setattr(c, field, value)
+    assert lib.acid_config_check(C.byref(c)) == status
+    assert L.last_error()
+    assert lib.acid_weights_bytes(C.byref(c)) == 0
+
+
+def test_null_arguments_rejected(lib):
+    assert lib.acid_config_check(None) == L.ACID_ERR_INVALID_ARG
+    st = L.GateStateC()
+    assert lib.acid_gate(C.byref(st), None, 0.0, None, None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_cache_apply(7, None, None, None, 4, None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_cache_apply(0, None, None, None, 0, None) == 0  # empty is a no-op
+
+
+def _c_gate_run(lib, s_seq, p):
+    st = L.GateStateC()
+    pc = L.GateParamsC(p.tau_low, p.tau_high, p.delta, p.n_warmup)
+    dec, taus, sums = [], [], []
+    comp, tau = C.c_int32(), C.c_double()
+    for s in s_seq:
+        assert lib.acid_gate(C.byref(st), C.byref(pc), float(s), C.byref(comp), C.byref(tau)) == 0
+        dec.append(bool(comp.value))
+        taus.append(tau.value)
+        sums.append(st.sigma_sum)
+    return dec, taus, sums
+
+
+def _same(a, b):
+    return all((x == y) or (math.isnan(x) and math.isnan(y)) for x, y in zip(a, b))
+
+
+def test_c_gate_dyadic_trace(lib):
+    s = [0.0, 0.03125, 0.03125, 0.0625, 0.078125, 0.078125, 0.09375, 0.09375, 0.0625, 0.125]
+    dec, _, sums = _c_gate_run(lib, s, O.GateParams(0.0625, 0.25, 0.015625, 1))
+    assert "".join("C" if d else "S" for d in dec) == "CSSCSSSCSC"
+    assert sums[6] == 0.25
+
+
+def test_c_gate_bit_exact_vs_oracle(lib):
+    """10^4 random sequences (with near-ties and NaN/inf) give identical
+    decisions, thresholds and accumulators in the C gate and the oracle."""
+    rng = np.random.default_rng(42)
+    for k in range(10000):
+        n = int(rng.integers(1, 40))
+        s = np.abs(rng.normal(0.04, 0.03, n))
+        if k % 7 == 0:  # exact repeats and deltas on the boundary
+            s = np.round(s * 64) / 64
+        if k % 97 == 0:
+            s[rng.integers(0, n)] = math.nan
+        if k % 89 == 0:
+            s[rng.integers(0, n)] = math.inf
+        p = O.GateParams(float(rng.choice([0.0, 0.05, 0.1, 0.0625])),
+                         float(rng.choice([0.1, 0.2, 0.25, math.inf])),
+                         float(rng.choice([-1.0, 0.0, 0.01, 0.015625, math.inf])),
+                         int(rng.integers(0, 3)))
+        d1, t1, s1 = O.gate_schedule(list(s), p)
+        d2, t2, s2 = _c_gate_run(lib, list(s), p)
+        assert d1 == d2, (k, list(s), p)
+        assert _same(t1, t2) and _same(s1, s2), k

@@ -1,0 +1,202 @@
+"""GPU parity of the individual kernels, through the C ABI, against the oracle.
+
+Sizes span several tiles plus ragged tails; bf16 inputs are compared with an
+oracle fed the same bf16-rounded values.  Tolerances: fp32 kernels 1e-5
+relative (Frobenius), bf16 attention/GEMM outputs 2e-2 (the bf16 bar) with
+typical errors far below it.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import acid_inputs as ai
+import oracle as O
+from gpu_util import bf16_values, need_gpu, rel_err, to_dev, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    return need_gpu()
+
+
+# ------------------------------------------------------------------ cache
+
+
+@pytest.mark.parametrize("n", [0, 1, 3, 4, 1001, 4096 * 3 + 2, 32760 * 1536])
+def test_cache_store_apply(P, n):
+    x = torch.randn(n, device="cuda")
+    h = torch.randn(n, device="cuda")
+    r = torch.empty(n, device="cuda")
+    P.cache_apply(P.ACID_CACHE_STORE, x, h, r)
+    xs, hs = to_np(x), to_np(h)
+    if n:
+        idx = np.random.default_rng(n).integers(0, n, min(n, 100000))
+        np.testing.assert_allclose(to_np(r)[idx], (hs - xs)[idx], rtol=1e-6, atol=1e-7)
+    h2 = torch.empty(n, device="cuda")
+    P.cache_apply(P.ACID_CACHE_APPLY, x, h2, r)
+    if n:
+        np.testing.assert_allclose(to_np(h2)[idx], hs[idx], rtol=1e-6, atol=1e-6)
+
+
+# ------------------------------------------------------- LN + modulation
+
+
+@pytest.mark.parametrize("rows,H", [(1, 256), (37, 1024), (300, 1536), (5, 3072), (0, 256)])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_ln_modulate(P, rows, H, out):
+    rng = np.random.default_rng(rows * 7 + H)
+    x = rng.normal(size=(rows, H)).astype(np.float32) * 2 + 0.5
+    shift = rng.normal(size=H).astype(np.float32) * 0.1
+    scale = rng.normal(size=H).astype(np.float32) * 0.1
+    dt = torch.bfloat16 if out == "bf16" else torch.float32
+    o = torch.empty((rows, H), dtype=dt, device="cuda")
+    P.ln_modulate(to_dev(x), to_dev(shift), to_dev(scale), o)
+    torch.cuda.synchronize()
+    if rows == 0:
+        return
+    ref = O.modulate(O.layer_norm(x), shift.astype(np.float64), scale.astype(np.float64))
+    tol = 1e-5 if out == "f32" else 4e-3
+    assert rel_err(to_np(o), ref) < tol
+    if out == "bf16":  # each element is the bf16 rounding of a value within fp32 error
+        assert np.max(np.abs(to_np(o) - ref) / (np.abs(ref) + 1e-3)) < 2 ** -7
+
+
+# -------------------------------------------------------------- attention
+
+
+def _attn_case(P, n_heads, L, d, dtype, std, seed):
+    rng = np.random.default_rng(seed)
+    q = rng.normal(size=(n_heads, L, d)).astype(np.float32) * std
+    k = rng.normal(size=(n_heads, L, d)).astype(np.float32) * std
+    v = rng.normal(size=(n_heads, L, d)).astype(np.float32)
+    if dtype == torch.bfloat16:
+        q, k, v = bf16_values(q), bf16_values(k), bf16_values(v)
+    vt_ld = ((L + 7) // 8) * 8
+    vt = np.zeros((n_heads, d, vt_ld), np.float32)
+    vt[:, :, :L] = v.transpose(0, 2, 1)
+    vt[:, :, L:] = np.nan  # padding must never reach the output
+    o = torch.empty((L, n_heads * d), dtype=dtype, device="cuda")
+    P.attention(to_dev(q, dtype), to_dev(k, dtype), to_dev(vt, dtype), o)
+    torch.cuda.synchronize()
+    return q, k, v, to_np(o)
+
+
+@pytest.mark.parametrize("L", [1, 63, 64, 65, 130, 300, 1000])
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("std", [1.0, 4.0])
+def test_attention_bf16(P, L, d, std):
+    nh = 2
+    q, k, v, o = _attn_case(P, nh, L, d, torch.bfloat16, std, seed=L * 131 + d + int(std))
+    assert np.all(np.isfinite(o))
+    for j in range(nh):
+        ref = O.attention(q[j], k[j], v[j])
+        got = o[:, j * d:(j + 1) * d]
+        e = rel_err(got, ref)
+        assert e < 2e-2, (j, e)
+        assert e < 1e-2  # typical bf16 P rounding error is ~3e-3
+
+
+@pytest.mark.parametrize("L", [1, 37, 128, 300])
+@pytest.mark.parametrize("d", [64, 128])
+def test_attention_f32(P, L, d):
+    nh = 3
+    q, k, v, o = _attn_case(P, nh, L, d, torch.float32, 1.0, seed=L + d)
+    for j in range(nh):
+        assert rel_err(o[:, j * d:(j + 1) * d], O.attention(q[j], k[j], v[j])) < 1e-5
+
+
+def test_attention_uniform_and_single_key(P):
+    """Q = 0 gives the mean of V; L = 1 returns V (properties at any size)."""
+    for L in (1, 777):
+        nh, d = 1, 128
+        v = np.random.default_rng(L).normal(size=(nh, L, d)).astype(np.float32)
+        v = bf16_values(v)
+        vt_ld = ((L + 7) // 8) * 8
+        vt = np.zeros((nh, d, vt_ld), np.float32)
+        vt[:, :, :L] = v.transpose(0, 2, 1)
+        q = torch.zeros((nh, L, d), dtype=torch.bfloat16, device="cuda")
+        k = to_dev(np.random.default_rng(1).normal(size=(nh, L, d)), torch.bfloat16)
+        o = torch.empty((L, d), dtype=torch.bfloat16, device="cuda")
+        P.attention(q, k, to_dev(vt, torch.bfloat16), o)
+        np.testing.assert_allclose(to_np(o), np.tile(v[0].mean(0), (L, 1)), atol=2e-2)
+
+
+# -------------------------------------------------------------------- GEMM
+
+KINDS = ["bias", "gelu", "gate_residual", "qkv", "euler"]
+
+
+def _linear_case(P, kind, M, N, K, dtype, seed):
+    rng = np.random.default_rng(seed)
+    a = rng.normal(size=(M, K)).astype(np.float32)
+    w = rng.normal(size=(K, N)).astype(np.float32) / math.sqrt(K)
+    b = rng.normal(size=N).astype(np.float32) * 0.1
+    if dtype == torch.bfloat16:
+        a, w = bf16_values(a), bf16_values(w)
+    y = a.astype(np.float64) @ w.astype(np.float64) + b
+    ad, wtd, bd = to_dev(a, dtype), to_dev(w.T.copy(), dtype), to_dev(b)
+    if kind == "bias":
+        out = torch.empty((M, N), device="cuda")
+        P.linear(ad, wtd, P.ACID_EPI_BIAS, bd, out=out)
+        return [(to_np(out), y, 1e-5)]
+    if kind == "gelu":
+        out = torch.empty((M, N), dtype=dtype, device="cuda")
+        P.linear(ad, wtd, P.ACID_EPI_BIAS_GELU, bd, out=out)
+        return [(to_np(out), O.gelu_tanh(y), 1e-5 if dtype == torch.float32 else 4e-3)]
+    if kind == "gate_residual":
+        h0 = rng.normal(size=(M, N)).astype(np.float32)
+        g = rng.normal(size=N).astype(np.float32)
+        h = to_dev(h0)
+        P.linear(ad, wtd, P.ACID_EPI_GATE_RESIDUAL, bd, gate=to_dev(g), out=h)
+        return [(to_np(h) - h0, g * y, 1e-5)]
+    if kind == "euler":
+        x0 = rng.normal(size=(M, N)).astype(np.float32)
+        x = to_dev(x0)
+        v = torch.empty((M, N), device="cuda")
+        P.linear(ad, wtd, P.ACID_EPI_EULER, bd, out=x, v_out=v, dsigma=-0.125)
+        return [(to_np(v), y, 1e-5), (to_np(x) - x0, -0.125 * y, 1e-5)]
+    # qkv: N = 3 * heads * d
+    d = 64
+    nh = N // (3 * d)
+    H = nh * d
+    vt_ld = ((M + 7) // 8) * 8
+    q = torch.empty((nh, M, d), dtype=dtype, device="cuda")
+    k = torch.empty((nh, M, d), dtype=dtype, device="cuda")
+    vt = torch.zeros((nh, d, vt_ld), dtype=dtype, device="cuda")
+    P.linear(ad, wtd, P.ACID_EPI_QKV, bd, q=q, k=k, vt=vt, n_heads=nh, head_dim=d)
+    tol = 1e-5 if dtype == torch.float32 else 4e-3
+    yq = y[:, :H].reshape(M, nh, d).transpose(1, 0, 2)
+    yk = y[:, H:2 * H].reshape(M, nh, d).transpose(1, 0, 2)
+    yv = y[:, 2 * H:].reshape(M, nh, d).transpose(1, 2, 0)
+    return [(to_np(q), yq, tol), (to_np(k), yk, tol), (to_np(vt)[:, :, :M], yv, tol)]
+
+
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("M,N,K", [(1, 384, 64), (255, 384, 128), (300, 768, 192), (600, 384, 320)])
+def test_linear(P, kind, dtype, M, N, K):
+    for got, ref, tol in _linear_case(P, kind, M, N, K, dtype, seed=M + N + K):
+        e = rel_err(got, ref)
+        assert e < tol, (kind, e)
+
+
+def test_linear_shape_errors(P):
+    a = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
+    wt = torch.zeros((100, 64), dtype=torch.bfloat16, device="cuda")
+    b = torch.zeros(100, device="cuda")
+    out = torch.zeros((4, 100), device="cuda")
+    with pytest.raises(P.AcidError) as ei:
+        P.linear(a, wt, P.ACID_EPI_BIAS, b, out=out)
+    assert ei.value.status == 2
+
+
+def test_linear_deterministic(P):
+    got = []
+    for _ in range(3):
+        (o, _, _), = _linear_case(P, "bias", 700, 1536, 1536, torch.bfloat16, seed=5)
+        got.append(o)
+    assert np.array_equal(got[0], got[1]) and np.array_equal(got[0], got[2])
