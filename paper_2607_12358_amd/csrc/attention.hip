@@ -32,9 +32,9 @@ struct AttnLds {
 };
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restrict__ Q,
-                                                           const bf16* __restrict__ Kp,
-                                                           const bf16* __restrict__ Vt,
+__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
+                                                           const bf16* Kp,
+                                                           const bf16* Vt,
                                                            int64_t L, int64_t vt_ld, int n_heads,
                                                            bf16* __restrict__ O,
                                                            float scale_log2) {
@@ -57,12 +57,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
   const bf16* Vh = Vt + (int64_t)head * D * vt_ld;
 
   bf16x8 qf[NK];
+  {
+    const bf16* qsrc = Qh + (qrow < L ? qrow : L - 1) * D + lg * 8;
+    const uint32_t qmask = qrow < L ? 0xFFFFFFFFu : 0u;
 #pragma unroll
-  for (int kk = 0; kk < NK; ++kk) {
-    if (qrow < L)
-      qf[kk] = *reinterpret_cast<const bf16x8*>(Qh + qrow * D + kk * 16 + lg * 8);
-    else
-      for (int i = 0; i < 8; ++i) qf[kk][i] = (bf16)0.f;
+    for (int kk = 0; kk < NK; ++kk) {
+      uint4 v = *reinterpret_cast<const uint4*>(qsrc + kk * 16);
+      v = make_uint4(v.x & qmask, v.y & qmask, v.z & qmask, v.w & qmask);
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
+    }
   }
 
   f32x16 o[ND];
@@ -72,55 +75,60 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -__builtin_inff(), l_run = 0.f;
 
-  uint4 rk[CPT], rv[CPT];
-  const uint4 zero4 = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int64_t j0) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i, row = c / (D / 8), cc = c % (D / 8);
-      const int64_t key = j0 + row;
-      rk[i] = key < L ? *reinterpret_cast<const uint4*>(Kh + key * D + cc * 8) : zero4;
-    }
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i, drow = c >> 3, cc = c & 7;
-      const int64_t key0 = j0 + cc * 8;
-      uint4 v = zero4;
-      if (key0 < L) {
-        v = *reinterpret_cast<const uint4*>(Vh + (int64_t)drow * vt_ld + key0);
-        const int64_t valid = L - key0;  // keys past L are zeroed
-        if (valid < 8) {
-          uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (e >= valid) w[e >> 1] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-          v = make_uint4(w[0], w[1], w[2], w[3]);
-        }
-      }
-      rv[i] = v;
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i, row = c / (D / 8), cc = c % (D / 8);
-      *reinterpret_cast<uint4*>(Ks + buf * Ld::K_ELEMS + row * KLD + cc * 8) = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int c = tid + 256 * i, drow = c >> 3, cc = c & 7;
-      *reinterpret_cast<uint4*>(Vs + buf * Ld::V_ELEMS + drow * VLD + cc * 8) = rv[i];
-    }
-  };
+  // Staging: thread tid moves chunk c = tid + 256 i of each tile.  K tile:
+  // row c / (D/8) (a key), chunk c % (D/8).  V^T tile: row c / 8 (a head dim),
+  // chunk c % 8 (8 keys).  Out-of-range keys read a valid address and are
+  // zeroed by value.
+  constexpr int KCH = D / 8;
+  u32x4 rk[CPT], rv[CPT];
+
+#define ATTN_GLOAD(J0)                                                                  \
+  do {                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
+      const int c_ = tid + 256 * i;                                                     \
+      const int64_t key_ = (J0) + c_ / KCH;                                             \
+      rk[i] = *reinterpret_cast<const u32x4*>(Kh + (key_ < L ? key_ : L - 1) * D +      \
+                                              (c_ % KCH) * 8);                          \
+    }                                                                                   \
+    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
+      const int c_ = tid + 256 * i;                                                     \
+      const int64_t key0_ = (J0) + (c_ & 7) * 8;                                        \
+      rv[i] = *reinterpret_cast<const u32x4*>(Vh + (int64_t)(c_ >> 3) * vt_ld +         \
+                                              (key0_ < L ? key0_ : 0));                 \
+    }                                                                                   \
+  } while (0)
+// Masks keys >= L (by value) while writing the staged tile J0 to LDS.
+#define ATTN_SSTORE(BUF, J0)                                                            \
+  do {                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
+      const int c_ = tid + 256 * i;                                                     \
+      const uint32_t m_ = ((J0) + c_ / KCH < L) ? 0xFFFFFFFFu : 0u;                     \
+      *reinterpret_cast<u32x4*>(Ks + (BUF) * Ld::K_ELEMS + (c_ / KCH) * KLD +           \
+                                (c_ % KCH) * 8) = rk[i] & m_;                           \
+      const int64_t key0_ = (J0) + (c_ & 7) * 8;                                        \
+      const int64_t valid_ = key0_ < L ? L - key0_ : 0;                                 \
+      u32x4 vm_;                                                                        \
+      _Pragma("unroll") for (int p_ = 0; p_ < 4; ++p_)                                  \
+        vm_[p_] = ((2 * p_ < valid_) ? 0x0000FFFFu : 0u) |                              \
+                  ((2 * p_ + 1 < valid_) ? 0xFFFF0000u : 0u);                           \
+      *reinterpret_cast<u32x4*>(Vs + (BUF) * Ld::V_ELEMS + (c_ >> 3) * VLD +            \
+                                (c_ & 7) * 8) = rv[i] & vm_;                            \
+    }                                                                                   \
+  } while (0)
 
   const int64_t nkv = (L + BKV - 1) / BKV;
-  gload(0);
-  sstore(0);
+  ATTN_GLOAD(0);
+  ATTN_SSTORE(0, 0);
   __syncthreads();
+  // Unconditional prefetch (the last tile reloads itself into the idle
+  // buffer): no branches around the staging registers.
   for (int64_t it = 0; it < nkv; ++it) {
     const int buf = (int)(it & 1);
     const int64_t j0 = it * BKV;
-    if (it + 1 < nkv) gload(j0 + BKV);
+    const int64_t jn = (it + 1 < nkv ? it + 1 : it) * BKV;
+    ATTN_GLOAD(jn);
+    asm volatile("" ::: "memory");     // no IR pass may sink the prefetch
+    __builtin_amdgcn_sched_barrier(0);  // nor the machine scheduler
 
     // S^T (keys x queries) for two 32-key blocks.
     f32x16 s[2];
@@ -184,9 +192,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* __restric
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][k2], o[db], 0, 0, 0);
       }
     }
-    if (it + 1 < nkv) sstore(buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);  // masks and LDS writes after the MFMAs
+    ATTN_SSTORE(buf ^ 1, jn);
     __syncthreads();
   }
+#undef ATTN_GLOAD
+#undef ATTN_SSTORE
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;

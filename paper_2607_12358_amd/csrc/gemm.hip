@@ -62,6 +62,60 @@ __device__ __forceinline__ void epi_elem(const Epi& e, int64_t m, int n, int N, 
   }
 }
 
+// Epilogue of one output column n: bias, gate and destination are resolved
+// once; put(m, acc) then stores row m.
+template <int KIND, typename T>
+struct ColEpi {
+  float bias, gate;
+  T* dst_t;
+  float* dst_f;
+  float* v_f;
+  int64_t stride;
+  float dsigma;
+  __device__ __forceinline__ ColEpi(const Epi& e, int n, int N) {
+    bias = e.bias[n];
+    gate = (KIND == ACID_EPI_GATE_RESIDUAL) ? e.gate[n] : 0.f;
+    dsigma = e.dsigma;
+    dst_t = nullptr;
+    dst_f = nullptr;
+    v_f = nullptr;
+    stride = N;
+    if constexpr (KIND == ACID_EPI_QKV) {
+      const int which = n / e.H, c = n - which * e.H;
+      const int head = c / e.head_dim, dd = c - head * e.head_dim;
+      if (which < 2) {
+        dst_t = static_cast<T*>(which == 0 ? e.q : e.k) + (int64_t)head * e.M * e.head_dim + dd;
+        stride = e.head_dim;
+      } else {
+        dst_t = static_cast<T*>(e.vt) + ((int64_t)head * e.head_dim + dd) * e.vt_ld;
+        stride = 1;
+      }
+    } else if constexpr (KIND == ACID_EPI_BIAS_GELU) {
+      dst_t = static_cast<T*>(e.out) + n;
+    } else {
+      dst_f = static_cast<float*>(e.out) + n;
+      if (KIND == ACID_EPI_EULER && e.v_out) v_f = e.v_out + n;
+    }
+  }
+  __device__ __forceinline__ void put(int64_t m, float acc) const {
+    const float y = acc + bias;
+    if constexpr (KIND == ACID_EPI_BIAS) {
+      dst_f[m * stride] = y;
+    } else if constexpr (KIND == ACID_EPI_BIAS_GELU) {
+      dst_t[m * stride] = (T)gelu_tanh(y);
+    } else if constexpr (KIND == ACID_EPI_GATE_RESIDUAL) {
+      float* h = dst_f + m * stride;
+      *h = *h + gate * y;
+    } else if constexpr (KIND == ACID_EPI_QKV) {
+      dst_t[m * stride] = (T)y;
+    } else {
+      if (v_f) v_f[m * stride] = y;
+      float* x = dst_f + m * stride;
+      *x = *x + dsigma * y;
+    }
+  }
+};
+
 // Bijection from dispatch order to tile order giving XCD x (workgroups
 // bid = x, x+8, ...) the contiguous tile range of its share.
 __device__ __forceinline__ int64_t xcd_remap(int64_t bid, int64_t T) {
@@ -91,8 +145,8 @@ constexpr int kLdsA = BM * LDK, kLdsB = BN * LDK;  // elements per buffer
 constexpr size_t kGemmLds = (size_t)2 * (kLdsA + kLdsB) * sizeof(bf16);
 
 template <int KIND>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* __restrict__ A,
-                                                           const bf16* __restrict__ Wt,
+__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* A,
+                                                           const bf16* Wt,
                                                            int64_t M, int N, int K, Epi e) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   bf16* As = reinterpret_cast<bf16*>(smem);
@@ -118,41 +172,51 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* __restric
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  uint4 ra[8], rb[4];
-  const uint4 zero4 = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int k0) {
+  // Global -> register staging.  Rows past M read row M-1 (a valid address)
+  // and are zeroed by value, so every load is an unconditional global load.
+  const int srow = tid >> 3, skc = tid & 7;  // row (+32 i) and 16-byte chunk
+  const bf16* a_src[8];
+  uint32_t a_mask[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-      const int64_t gm = m0 + row;
-      ra[i] = gm < M ? *reinterpret_cast<const uint4*>(A + gm * K + k0 + kc * 8) : zero4;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-      rb[i] = *reinterpret_cast<const uint4*>(Wt + (int64_t)(n0 + row) * K + k0 + kc * 8);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-      *reinterpret_cast<uint4*>(As + buf * kLdsA + row * LDK + kc * 8) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-      *reinterpret_cast<uint4*>(Bs + buf * kLdsB + row * LDK + kc * 8) = rb[i];
-    }
-  };
+  for (int i = 0; i < 8; ++i) {
+    const int64_t gm = m0 + srow + 32 * i;
+    a_mask[i] = gm < M ? 0xFFFFFFFFu : 0u;
+    a_src[i] = A + (gm < M ? gm : M - 1) * K + skc * 8;
+  }
+  const bf16* b_src = Wt + (int64_t)(n0 + srow) * K + skc * 8;
+  u32x4 ra[8], rb[4];
 
-  gload(0);
-  sstore(0);
+#define GEMM_GLOAD(K0)                                                              \
+  do {                                                                              \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                 \
+      ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + (K0));                     \
+    }                                                                               \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                   \
+      rb[i] = *reinterpret_cast<const u32x4*>(b_src + (int64_t)32 * i * K + (K0));  \
+  } while (0)
+#define GEMM_SSTORE(BUF)                                                            \
+  do {                                                                              \
+    bf16* as_ = As + (BUF) * kLdsA + srow * LDK + skc * 8;                          \
+    bf16* bs_ = Bs + (BUF) * kLdsB + srow * LDK + skc * 8;                          \
+    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                   \
+      *reinterpret_cast<u32x4*>(as_ + 32 * i * LDK) = ra[i] & a_mask[i];            \
+    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                   \
+      *reinterpret_cast<u32x4*>(bs_ + 32 * i * LDK) = rb[i];                        \
+  } while (0)
+
+  GEMM_GLOAD(0);
+  GEMM_SSTORE(0);
   __syncthreads();
   const int KT = K / BK;
+  // The prefetch is unconditional (the last step reloads its own tile into
+  // the idle buffer) so the loop body has no branches and the staging
+  // registers stay in registers; masks are applied when writing LDS, after
+  // the MFMAs, so no wait on the loads is forced early.
   for (int kt = 0; kt < KT; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * BK);
+    GEMM_GLOAD((kt + 1 < KT ? kt + 1 : kt) * BK);
+    asm volatile("" ::: "memory");     // no IR pass may sink the prefetch
+    __builtin_amdgcn_sched_barrier(0);  // nor the machine scheduler
     const bf16* Ab = As + buf * kLdsA + (wm * 128 + lr) * LDK + lg * 8;
     const bf16* Bb = Bs + buf * kLdsB + (wn * 64 + lr) * LDK + lg * 8;
 #pragma unroll
@@ -170,22 +234,27 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* __restric
         for (int nb = 0; nb < 2; ++nb)
           acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
     }
-    if (kt + 1 < KT) sstore(buf ^ 1);
+    __builtin_amdgcn_sched_barrier(0);  // masks and LDS writes after the MFMAs
+    GEMM_SSTORE(buf ^ 1);
     __syncthreads();
   }
+#undef GEMM_GLOAD
+#undef GEMM_SSTORE
 
   // D[i][j] of a 32x32 block: j = lane % 32, i = 8 (r / 4) + 4 (lane / 32) + r % 4.
+  // A lane owns one feature column per 32-wide block: set up its epilogue once.
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int nb = 0; nb < 2; ++nb) {
+    const int n = n0 + wn * 64 + nb * 32 + lr;
+    ColEpi<KIND, bf16> ce(e, n, N);
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int n = n0 + wn * 64 + nb * 32 + lr;
+    for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t m = m0 + wm * 128 + mb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
-        if (m < M) epi_elem<KIND, bf16>(e, m, n, N, acc[mb][nb][r]);
+        if (m < M) ce.put(m, acc[mb][nb][r]);
       }
-    }
+  }
 }
 
 // ------------------------------------------------------------ fp32 VALU
