@@ -61,9 +61,9 @@ typedef enum { ACID_MODE_NOCACHE = 0, ACID_MODE_ACID = 1 } acid_mode;
 typedef enum { ACID_CACHE_STORE = 0, ACID_CACHE_APPLY = 1 } acid_cache_op;
 
 /* Shape of the DiT stack.  Token rows are ordered text first, then video.
- * hidden = n_heads * head_dim.  Supported: head_dim 64 or 128; hidden, 3
- * hidden and ffn multiples of 128; hidden and ffn multiples of 64 (GEMM K);
- * freq_dim even and <= 1024. */
+ * hidden = n_heads * head_dim.  Supported: head_dim 64 or 128; hidden
+ * (<= 4096) and ffn multiples of 128 (every GEMM's N and K); freq_dim even
+ * and <= 1024. */
 typedef struct {
   int32_t n_blocks;
   int32_t hidden;
@@ -291,7 +291,7 @@ typedef struct {
 } acid_epilogue_args;
 
 /* Fused GEMM: a [M][K] and wt = W transposed [N][K], both in `dtype`;
- * N % 128 == 0, K % 64 == 0, any M >= 0. */
+ * N % 128 == 0, K % 128 == 0, any M >= 0 (ACID_ERR_SHAPE otherwise). */
 acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K,
                         const void* a_dev, const void* wt_dev,
                         const acid_epilogue_args* epi, hipStream_t stream);

@@ -143,36 +143,52 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
       }
     }
-    // Scale into the exp2 domain, mask keys past L, row max.
-    float mx = -__builtin_inff();
+    // Keys past L exist only in the last tile: mask them there (uniform branch).
+    if (j0 + BKV > L) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t key = j0 + kb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+          if (key >= L) s[kb][r] = -__builtin_inff();
+        }
+    }
+    // Row max of the raw scores (scale > 0 commutes with max), shared with
+    // the partner half-wave that holds the other keys of the same query.
+    float mx = s[0][0];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t key = j0 + kb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
-        const float v = key < L ? s[kb][r] * scale_log2 : -__builtin_inff();
-        s[kb][r] = v;
-        mx = fmaxf(mx, v);
-      }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
-    m_run = m_new;
+    // Lazy rescaling: the running reference max moves only when the new
+    // max exceeds it by more than 2^8 in probability, so probabilities stay
+    // <= 256 (exact range for bf16 and fp32) and the O / l rescale is skipped
+    // on most tiles.  The branch is wave-uniform.
+    const float m_cand = mx * scale_log2;
+    const bool grow = m_cand > m_run + 8.0f;
+    if (__any(grow)) {
+      const float m_new = grow ? m_cand : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < ND; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+    }
+    // p = 2^(s log2(e)/sqrt(d) - m): one FMA and one v_exp_f32 per score.
     float psum = 0.f;
     bf16x8 pf[2][2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[kb][r] - m_new);
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][r], scale_log2, -m_run));
         psum += p;
         pf[kb][r >> 3][r & 7] = (bf16)p;
       }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int db = 0; db < ND; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+    l_run += psum;
 
     // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
     // (kb, k2) is key kb*32 + 16 k2 + 8 (e / 4) + 4 lg + e % 4, matching the

@@ -50,6 +50,15 @@ __device__ __forceinline__ float gelu_tanh(float z) {
   return 0.5f * z * (1.0f + tanhf(u));
 }
 
+// Same function for bf16 outputs: 0.5 z (1 + tanh(u)) == z / (1 + e^(-2u)),
+// one exp2 and one reciprocal (hardware approximations, ~1 ulp each).
+__device__ __forceinline__ float gelu_tanh_fast(float z) {
+  // -2 log2(e) sqrt(2/pi)
+  const float k = -2.302208198144325f;
+  const float t = k * z * __builtin_fmaf(0.044715f * z, z, 1.0f);
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(t));
+}
+
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }

@@ -2,12 +2,17 @@
 // needs (plain, tanh-GELU, gated residual add, QKV head split, Euler update).
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (gfx950), fp32 accumulate.
-//   Macro tile 256 (tokens) x 128 (features) x 64 (K), 4 waves in a 2x2
-//   grid, each wave 128 x 64 = 4 x 2 MFMA blocks of 32 x 32.  Both operands
-//   are staged K-contiguous in LDS (rows padded by 16 bytes so that a
-//   half-wave's 16-byte fragment reads hit distinct banks), double-buffered
-//   with register prefetch so global loads of tile k+1 overlap the MFMAs of
-//   tile k, one barrier per K step.  The activation tile feeds MFMA operand A
+//   Macro tile 256 (tokens) x 256 (features), K in steps of 64, 4 waves in a
+//   2x2 grid, each wave 128 x 128 = 4 x 4 MFMA blocks of 32 x 32
+//   (accumulators in AGPRs).  Operands go global -> LDS directly
+//   (global_load_lds_dwordx4, no staging registers) into two 64 KB stages,
+//   K-contiguous 128-byte rows (whole cache lines, so the L2 request rate
+//   stays within budget) with an XOR swizzle that is conflict-free for
+//   gfx950's 64 LDS banks.  One barrier per K-step, placed before the last
+//   16-wide sub-step so the refill DMA and the next stage's first fragment
+//   reads hide behind its MFMAs; all other fragment reads are
+//   software-pipelined one sub-step ahead.  A 256 x 256 tile halves the
+//   operand bytes per flop of a 256 x 128 tile.  The activation tile feeds MFMA operand A
 //   and the weight tile operand B, so the accumulator holds C with lanes
 //   along features: every epilogue store is a run of consecutive features of
 //   one token row (coalesced), and bias / gate are one value per lane.
@@ -97,12 +102,32 @@ struct ColEpi {
       if (KIND == ACID_EPI_EULER && e.v_out) v_f = e.v_out + n;
     }
   }
+  static constexpr bool kRmw = KIND == ACID_EPI_GATE_RESIDUAL || KIND == ACID_EPI_EULER;
+  // Read-modify-write kinds read the old value first (batched by the caller).
+  __device__ __forceinline__ float old(int64_t m) const {
+    if constexpr (kRmw) return dst_f[m * stride];
+    return 0.f;
+  }
+  __device__ __forceinline__ void put_old(int64_t m, float acc, float prev) const {
+    const float y = acc + bias;
+    if constexpr (KIND == ACID_EPI_GATE_RESIDUAL) {
+      dst_f[m * stride] = prev + gate * y;
+    } else if constexpr (KIND == ACID_EPI_EULER) {
+      if (v_f) v_f[m * stride] = y;
+      dst_f[m * stride] = prev + dsigma * y;
+    } else {
+      put(m, acc);
+    }
+  }
   __device__ __forceinline__ void put(int64_t m, float acc) const {
     const float y = acc + bias;
     if constexpr (KIND == ACID_EPI_BIAS) {
       dst_f[m * stride] = y;
     } else if constexpr (KIND == ACID_EPI_BIAS_GELU) {
-      dst_t[m * stride] = (T)gelu_tanh(y);
+      if constexpr (sizeof(T) == 2)
+        dst_t[m * stride] = (T)gelu_tanh_fast(y);
+      else
+        dst_t[m * stride] = (T)gelu_tanh(y);
     } else if constexpr (KIND == ACID_EPI_GATE_RESIDUAL) {
       float* h = dst_f + m * stride;
       *h = *h + gate * y;
@@ -140,19 +165,75 @@ __device__ __forceinline__ void tile_coords(int64_t t, int64_t tiles_m, int tile
 
 // ------------------------------------------------------------ bf16 MFMA
 
-constexpr int BM = 256, BN = 128, BK = 64, LDK = BK + 8;
-constexpr int kLdsA = BM * LDK, kLdsB = BN * LDK;  // elements per buffer
-constexpr size_t kGemmLds = (size_t)2 * (kLdsA + kLdsB) * sizeof(bf16);
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int kTileElems = 256 * BK;  // one operand tile per stage (32 KB)
+
+// One 256 x 64 operand tile (rows K-contiguous, 128 B = 8 chunks of 16 B per
+// row; every row fetch is one whole 128-byte line, which halves the L2
+// request rate of narrower K-steps) moved global -> LDS with
+// global_load_lds_dwordx4.  Instruction i of wave w fills LDS bytes
+// [(8 w + i) KB, +1 KB) = rows 64 w + 8 i .. +7; lane l lands in row
+// 64 w + 8 i + l / 8, slot l % 8, which holds global chunk
+// (l % 8) ^ ((row / 2) % 8).  With 64 four-byte LDS banks a row spans half
+// the banks, so 16 consecutive fragment rows read at one chunk cover all 64
+// banks exactly once.
+// Issued as inline assembly so the compiler's wait-count pass does not see
+// the LDS-DMA (it cannot order DMA completions against LDS reads and would
+// drain every read).  Completion is tracked explicitly with vmcnt waits; M0
+// (the DMA's LDS base) is set here and the compiler issues no other M0 user
+// in this kernel.
+__device__ __forceinline__ void load_tile_lds(bf16* lds_tile, const bf16* const (&row_ptr)[8],
+                                              int chunk_even, int chunk_odd, int k0, int wave) {
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(lds_void_t*)(lds_tile + (wave * 8) * 512));
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const bf16* g = row_ptr[i] + k0 + ((i & 1) ? chunk_odd : chunk_even) * 8;
+    asm volatile(
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %0, off"
+        :
+        : "v"(g), "s"(lds0 + i * 1024)
+        : "memory");
+  }
+}
+
+// One 16-byte-per-lane LDS-DMA (see load_tile_lds).
+__device__ __forceinline__ void dma16(const bf16* g, uint32_t lds_byte) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(g), "s"(lds_byte)
+      : "memory");
+}
+
+// Waits until at most N of this wave's global loads are outstanding.  The
+// main loop pairs it with a bare s_barrier (no fence: __syncthreads would
+// also drain every in-flight prefetch): a wave's own LDS-DMA writes are
+// complete after the wait, everyone's after the barrier.
+// gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
 
 template <int KIND>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* A,
-                                                           const bf16* Wt,
+__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* A, const bf16* Wt,
                                                            int64_t M, int N, int K, Epi e) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  bf16* As = reinterpret_cast<bf16*>(smem);
-  bf16* Bs = As + 2 * kLdsA;
+  // Two stages of A and B tiles, one LDS object per tile so the compiler can
+  // tell the stage being read from the stage being filled.
+  __shared__ __attribute__((aligned(1024))) bf16 As0[kTileElems], Bs0[kTileElems];
+  __shared__ __attribute__((aligned(1024))) bf16 As1[kTileElems], Bs1[kTileElems];
 
-  const int tiles_n = N / BN;
+  const int tiles_n = (N + BN - 1) / BN;
   const int64_t tiles_m = (M + BM - 1) / BM;
   int64_t tm;
   int tn;
@@ -163,97 +244,177 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* A,
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int lr = lane & 31, lg = lane >> 5;
+  // A tile of width 128 at the right edge (N % 256 == 128): waves with wn = 1
+  // compute on clamped rows and store nothing.
+  const bool active = n0 + wn * 128 < N;
 
-  f32x16 acc[4][2];
+  // Load-side addressing (rows past the edge are clamped: they only feed
+  // outputs that are never stored).
+  const int chunk_even = (lane & 7) ^ (lane >> 4);
+  const int chunk_odd = (lane & 7) ^ ((lane >> 4) ^ 4);
+  const bf16* a_row[8];
+  const bf16* b_row[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = wave * 64 + i * 8 + (lane >> 3);
+    const int64_t gm = m0 + r < M ? m0 + r : M - 1;
+    const int gn = n0 + r < N ? n0 + r : N - 1;
+    a_row[i] = A + gm * K;
+    b_row[i] = Wt + (int64_t)gn * K;
+  }
+
+  // Read-side addressing: fragment row rr at K-step kk (16 wide) reads chunk
+  // 2 kk + lg, stored at slot (2 kk + lg) ^ ((rr / 2) % 8), and
+  // (rr / 2) % 8 == (lr / 2) % 8 for every fragment row of this lane.
+  const int a_base = (wm * 128 + lr) * BK;
+  const int b_base = (wn * 128 + lr) * BK;
+  int sl[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) sl[kk] = 8 * ((2 * kk + lg) ^ ((lr >> 1) & 7));
+
+  f32x16 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Global -> register staging.  Rows past M read row M-1 (a valid address)
-  // and are zeroed by value, so every load is an unconditional global load.
-  const int srow = tid >> 3, skc = tid & 7;  // row (+32 i) and 16-byte chunk
-  const bf16* a_src[8];
-  uint32_t a_mask[8];
+  bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+  auto read_frags = [&](const bf16* As, const bf16* Bs, int slot, bf16x8 (&fa)[4],
+                        bf16x8 (&fb)[4]) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int64_t gm = m0 + srow + 32 * i;
-    a_mask[i] = gm < M ? 0xFFFFFFFFu : 0u;
-    a_src[i] = A + (gm < M ? gm : M - 1) * K + skc * 8;
-  }
-  const bf16* b_src = Wt + (int64_t)(n0 + srow) * K + skc * 8;
-  u32x4 ra[8], rb[4];
-
-#define GEMM_GLOAD(K0)                                                              \
-  do {                                                                              \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i) {                                 \
-      ra[i] = *reinterpret_cast<const u32x4*>(a_src[i] + (K0));                     \
-    }                                                                               \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                   \
-      rb[i] = *reinterpret_cast<const u32x4*>(b_src + (int64_t)32 * i * K + (K0));  \
-  } while (0)
-#define GEMM_SSTORE(BUF)                                                            \
-  do {                                                                              \
-    bf16* as_ = As + (BUF) * kLdsA + srow * LDK + skc * 8;                          \
-    bf16* bs_ = Bs + (BUF) * kLdsB + srow * LDK + skc * 8;                          \
-    _Pragma("unroll") for (int i = 0; i < 8; ++i)                                   \
-      *reinterpret_cast<u32x4*>(as_ + 32 * i * LDK) = ra[i] & a_mask[i];            \
-    _Pragma("unroll") for (int i = 0; i < 4; ++i)                                   \
-      *reinterpret_cast<u32x4*>(bs_ + 32 * i * LDK) = rb[i];                        \
-  } while (0)
-
-  GEMM_GLOAD(0);
-  GEMM_SSTORE(0);
-  __syncthreads();
-  const int KT = K / BK;
-  // The prefetch is unconditional (the last step reloads its own tile into
-  // the idle buffer) so the loop body has no branches and the staging
-  // registers stay in registers; masks are applied when writing LDS, after
-  // the MFMAs, so no wait on the loads is forced early.
-  for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    GEMM_GLOAD((kt + 1 < KT ? kt + 1 : kt) * BK);
-    asm volatile("" ::: "memory");     // no IR pass may sink the prefetch
-    __builtin_amdgcn_sched_barrier(0);  // nor the machine scheduler
-    const bf16* Ab = As + buf * kLdsA + (wm * 128 + lr) * LDK + lg * 8;
-    const bf16* Bb = Bs + buf * kLdsB + (wn * 64 + lr) * LDK + lg * 8;
+    for (int mb = 0; mb < 4; ++mb)
+      fa[mb] = *reinterpret_cast<const bf16x8*>(As + a_base + mb * 32 * BK + slot);
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[4], bfr[2];
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-        af[mb] = *reinterpret_cast<const bf16x8*>(Ab + mb * 32 * LDK + kk * 16);
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        bfr[nb] = *reinterpret_cast<const bf16x8*>(Bb + nb * 32 * LDK + kk * 16);
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-          acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mb], bfr[nb], acc[mb][nb], 0, 0, 0);
-    }
-    __builtin_amdgcn_sched_barrier(0);  // masks and LDS writes after the MFMAs
-    GEMM_SSTORE(buf ^ 1);
-    __syncthreads();
-  }
-#undef GEMM_GLOAD
-#undef GEMM_SSTORE
-
-  // D[i][j] of a 32x32 block: j = lane % 32, i = 8 (r / 4) + 4 (lane / 32) + r % 4.
-  // A lane owns one feature column per 32-wide block: set up its epilogue once.
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int n = n0 + wn * 64 + nb * 32 + lr;
-    ColEpi<KIND, bf16> ce(e, n, N);
+    for (int nb = 0; nb < 4; ++nb)
+      fb[nb] = *reinterpret_cast<const bf16x8*>(Bs + b_base + nb * 32 * BK + slot);
+  };
+  auto mma = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4]) {
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + wm * 128 + mb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
-        if (m < M) ce.put(m, acc[mb][nb][r]);
+      for (int nb = 0; nb < 4; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+  };
+
+  const int KT = K / BK;  // even: K % 128 == 0
+  // Prologue: stages 0 and 1 in flight, stage 0 landed, first fragments read.
+  load_tile_lds(As0, a_row, chunk_even, chunk_odd, 0, wave);
+  load_tile_lds(Bs0, b_row, chunk_even, chunk_odd, 0, wave);
+  load_tile_lds(As1, a_row, chunk_even, chunk_odd, BK, wave);
+  load_tile_lds(Bs1, b_row, chunk_even, chunk_odd, BK, wave);
+  wait_vmcnt<16>();
+  __builtin_amdgcn_s_barrier();
+  read_frags(As0, Bs0, sl[0], fa0, fb0);
+
+  // Stage kt (buffer kt % 2): K-steps 0..2 with the next step's fragments
+  // read behind each MFMA group; then this wave's reads of the buffer are
+  // done and stage kt+1 has landed (waits), barrier (everyone's are),
+  // refill this buffer with stage kt+2 and read stage kt+1's first
+  // fragments, both hidden behind K-step 3's MFMAs.  Past the last stage the
+  // refill reloads stage KT-1 into a buffer that is never read again.
+  // The refill of one stage is 16 DMA instructions per wave (8 for A, 8 for
+  // B).  Issuing them back to back stalls the wave on the memory pipe while
+  // the MFMA unit idles, so they are interleaved one per MFMA of the last
+  // sub-step (ordering pinned with scheduling barriers).
+  auto mma_refill = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4], bf16* As, bf16* Bs,
+                        int kn) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(lds_void_t*)(As + (wave * 8) * 512));
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(lds_void_t*)(Bs + (wave * 8) * 512));
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+        const int j = mb * 4 + nb, i = j & 7;
+        const int ch = (i & 1) ? chunk_odd : chunk_even;
+        if (j < 8)
+          dma16(a_row[i] + kn + ch * 8, la + i * 1024);
+        else
+          dma16(b_row[i] + kn + ch * 8, lb + i * 1024);
+        __builtin_amdgcn_sched_barrier(0);
       }
+  };
+
+  // Stage kt (buffer kt % 2): K-steps 0..2 with the next step's fragments
+  // read behind each MFMA group; then this wave's reads of the buffer are
+  // done and stage kt+1 has landed (wait), barrier (everyone's are), read
+  // stage kt+1's first fragments and run K-step 3 with the refill of this
+  // buffer (stage kt+2) interleaved.  Past the last stage the refill reloads
+  // stage KT-1 into a buffer that is never read again.
+#define GEMM_STAGE(AS, BS, AN, BN_)                                              \
+  {                                                                            \
+    read_frags(AS, BS, sl[1], fa1, fb1);                                       \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma(fa0, fb0);                                                             \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    read_frags(AS, BS, sl[2], fa0, fb0);                                       \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma(fa1, fb1);                                                             \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    read_frags(AS, BS, sl[3], fa1, fb1);                                       \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma(fa0, fb0);                                                             \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    wait_all();                                                                \
+    __builtin_amdgcn_s_barrier();                                              \
+    read_frags(AN, BN_, sl[0], fa0, fb0);                                      \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma_refill(fa1, fb1, AS, BS, (kt + 2 < KT ? kt + 2 : KT - 1) * BK);        \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+  }
+  for (int kt = 0; kt < KT; kt += 2) {
+    GEMM_STAGE(As0, Bs0, As1, Bs1)
+    ++kt;
+    GEMM_STAGE(As1, Bs1, As0, Bs0)
+    --kt;
+  }
+#undef GEMM_STAGE
+  if (!active) return;
+
+  // D[i][j] of a 32x32 block: j = lane % 32, i = 8 (r / 4) + 4 (lane / 32) + r % 4.
+  // A lane owns one feature column per 32-wide block: set up its epilogue
+  // once, then handle its 64 rows of that column.  Full tiles skip the row
+  // check (a per-element branch would serialise every load behind a wait);
+  // read-modify-write kinds issue all 64 loads before any store.
+  const bool full = m0 + BM <= M;
+  const int64_t mrow = m0 + wm * 128 + 4 * lg;
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    const int n = n0 + wn * 128 + nb * 32 + lr;
+    ColEpi<KIND, bf16> ce(e, n, N);
+    if (full) {
+      if constexpr (ColEpi<KIND, bf16>::kRmw) {
+        float prev[4][16];
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            prev[mb][r] = ce.old(mrow + mb * 32 + 8 * (r >> 2) + (r & 3));
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            ce.put_old(mrow + mb * 32 + 8 * (r >> 2) + (r & 3), acc[mb][nb][r], prev[mb][r]);
+      } else {
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            ce.put(mrow + mb * 32 + 8 * (r >> 2) + (r & 3), acc[mb][nb][r]);
+      }
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t m = mrow + mb * 32 + 8 * (r >> 2) + (r & 3);
+          if (m < M) ce.put(m, acc[mb][nb][r]);
+        }
+    }
   }
 }
 
@@ -310,16 +471,8 @@ template <int KIND>
 hipError_t launch_kind(int dtype, int64_t M, int N, int K, const void* a, const void* wt,
                        const Epi& e, hipStream_t s) {
   if (dtype == ACID_BF16) {
-    static bool attr_set = false;
-    if (!attr_set) {
-      hipError_t err = hipFuncSetAttribute((const void*)gemm_bf16_kernel<KIND>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)kGemmLds);
-      if (err != hipSuccess) return err;
-      attr_set = true;
-    }
-    const int64_t tiles = ((M + BM - 1) / BM) * (N / BN);
-    hipLaunchKernelGGL(gemm_bf16_kernel<KIND>, dim3((unsigned)tiles), dim3(256), kGemmLds, s,
+    const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    hipLaunchKernelGGL(gemm_bf16_kernel<KIND>, dim3((unsigned)tiles), dim3(256), 0, s,
                        (const bf16*)a, (const bf16*)wt, M, N, K, e);
   } else {
     dim3 grid((unsigned)((M + 63) / 64), (unsigned)(N / 64));

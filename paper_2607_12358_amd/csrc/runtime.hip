@@ -587,8 +587,8 @@ acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K, const vo
     return set_error(ACID_ERR_INVALID_ARG, "bad dtype %d", dtype);
   if (!epi) return set_error(ACID_ERR_INVALID_ARG, "epilogue args NULL");
   if (M < 0 || N <= 0 || K <= 0) return set_error(ACID_ERR_INVALID_ARG, "bad M/N/K");
-  if (N % 128 || K % 64)
-    return set_error(ACID_ERR_SHAPE, "N %d must be a multiple of 128 and K %d of 64", N, K);
+  if (N % 128 || K % 128)
+    return set_error(ACID_ERR_SHAPE, "N %d and K %d must be multiples of 128", N, K);
   if (M == 0) return ACID_OK;
   if (!a_dev || !wt_dev || !epi->bias) return set_error(ACID_ERR_INVALID_ARG, "NULL operand or bias");
   switch (epi->kind) {

@@ -177,7 +177,7 @@ def _linear_case(P, kind, M, N, K, dtype, seed):
 
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
-@pytest.mark.parametrize("M,N,K", [(1, 384, 64), (255, 384, 128), (300, 768, 192), (600, 384, 320)])
+@pytest.mark.parametrize("M,N,K", [(1, 384, 128), (255, 384, 256), (300, 768, 384), (600, 384, 640), (513, 1152, 1536)])
 def test_linear(P, kind, dtype, M, N, K):
     for got, ref, tol in _linear_case(P, kind, M, N, K, dtype, seed=M + N + K):
         e = rel_err(got, ref)
@@ -185,12 +185,16 @@ def test_linear(P, kind, dtype, M, N, K):
 
 
 def test_linear_shape_errors(P):
-    a = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
-    wt = torch.zeros((100, 64), dtype=torch.bfloat16, device="cuda")
+    a = torch.zeros((4, 128), dtype=torch.bfloat16, device="cuda")
+    wt = torch.zeros((100, 128), dtype=torch.bfloat16, device="cuda")
     b = torch.zeros(100, device="cuda")
     out = torch.zeros((4, 100), device="cuda")
     with pytest.raises(P.AcidError) as ei:
         P.linear(a, wt, P.ACID_EPI_BIAS, b, out=out)
+    assert ei.value.status == 2
+    wt = torch.zeros((128, 64), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(P.AcidError) as ei:
+        P.linear(a[:, :64].contiguous(), wt, P.ACID_EPI_BIAS, b[:128], out=out[:, :128].contiguous())
     assert ei.value.status == 2
 
 
