@@ -115,6 +115,9 @@ def main() -> int:
     ap.add_argument("--no-nocache", action="store_true", help="skip the uncached context loop")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="disable the per-kernel event timer")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run the residual-cache store over three 1 GiB fp32 arrays (reads "
+                         "2 GiB, writes 1 GiB): the reference for scaling HBM byte counters")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -128,6 +131,18 @@ def main() -> int:
 
     import acid_inputs as ai
     import paper_2607_12358_amd as P
+
+    if args.copy_calibration:
+        n = 1 << 28
+        x = torch.randn(n, device="cuda")
+        h = torch.randn(n, device="cuda")
+        r = torch.empty(n, device="cuda")
+        torch.cuda.synchronize()
+        P.cache_apply(P.ACID_CACHE_STORE, x, h, r)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration": {"elements": n, "read_bytes": 8 * n,
+                                               "write_bytes": 4 * n}}), flush=True)
+        return 0
 
     cfg = ai.CONFIGS[args.workload]
     if args.n_steps:

@@ -9,8 +9,11 @@
 //   the row sum stays a per-lane partial until the end.  The probabilities
 //   P^T in accumulator layout are exactly the B operand of O^T = V^T P^T when
 //   the contraction index is relabelled accordingly, so P never leaves
-//   registers; V is stored transposed (keys contiguous) by the QKV epilogue
-//   so the matching A operand is two 8-byte LDS reads.  Softmax runs in the
+//   registers; V is stored transposed (keys contiguous) by the QKV epilogue,
+//   and keys are staged into LDS in a permuted order so the matching A
+//   operand is one 16-byte read from an XOR-swizzled V^T tile (no LDS bank
+//   conflicts).  Work items are mapped so each XCD streams a contiguous,
+//   head-major range (a head's K/V passes through few L2s).  Softmax runs in the
 //   exp2 domain with log2(e)/sqrt(d) folded into one multiply, in fp32.
 // fp32 path: one thread per query with K/V tiles in LDS, online softmax in
 //   fp32 (for the fp32 configuration).
@@ -24,12 +27,30 @@ constexpr int BQ = 128, BKV = 64;
 
 template <int D>
 struct AttnLds {
-  static constexpr int KLD = D + 8;     // K tile row stride (elements)
-  static constexpr int VLD = BKV + 8;   // V^T tile row stride
+  static constexpr int KLD = D + 8;     // K tile row stride (elements), padded
+  static constexpr int VLD = BKV;       // V^T tile row stride: 128 B, XOR-swizzled
   static constexpr int K_ELEMS = BKV * KLD;
   static constexpr int V_ELEMS = D * VLD;
   static constexpr size_t BYTES = (size_t)2 * (K_ELEMS + V_ELEMS) * sizeof(bf16);
 };
+
+// Keys are staged into the K tile in the order pi(j) = j with bits 2 and 3
+// swapped (an involution).  Then the 8 probabilities a lane feeds to one
+// P V^T MFMA step are 8 consecutive keys, so the matching V^T operand is one
+// 16-byte LDS read.
+__device__ __forceinline__ int key_perm(int j) {
+  return (j & ~12) | ((j & 4) << 1) | ((j & 8) >> 1);
+}
+
+// Bijection from dispatch order to (head, query-tile) work items that gives
+// XCD x (workgroups bid = x, x+8, ...) a contiguous, head-major range, so a
+// head's K/V is streamed through as few L2s as possible.
+__device__ __forceinline__ int64_t attn_xcd_remap(int64_t bid, int64_t T) {
+  constexpr int64_t NX = 8;
+  const int64_t x = bid % NX, local = bid / NX;
+  const int64_t q = T / NX, r = T % NX;
+  return (x < r) ? x * (q + 1) + local : r * (q + 1) + (x - r) * q + local;
+}
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
@@ -47,10 +68,13 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
   bf16* Ks = reinterpret_cast<bf16*>(smem);
   bf16* Vs = Ks + 2 * Ld::K_ELEMS;
 
-  const int head = blockIdx.y;
+  const int64_t n_qt = (L + BQ - 1) / BQ;
+  const int64_t item = attn_xcd_remap(blockIdx.x, n_qt * n_heads);
+  const int head = (int)(item / n_qt);
+  const int64_t qt = item - (int64_t)head * n_qt;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lg = lane >> 5;
-  const int64_t qrow = (int64_t)blockIdx.x * BQ + wave * 32 + lr;
+  const int64_t qrow = qt * BQ + wave * 32 + lr;
 
   const bf16* Qh = Q + (int64_t)head * L * D;
   const bf16* Kh = Kp + (int64_t)head * L * D;
@@ -76,56 +100,69 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
   float m_run = -__builtin_inff(), l_run = 0.f;
 
   // Staging: thread tid moves chunk c = tid + 256 i of each tile.  K tile:
-  // row c / (D/8) (a key), chunk c % (D/8).  V^T tile: row c / 8 (a head dim),
-  // chunk c % 8 (8 keys).  Out-of-range keys read a valid address and are
-  // zeroed by value.
+  // key c / (D/8) into row key_perm(key), chunk c % (D/8).  V^T tile: row
+  // c / 8 (a head dim d), 8-key chunk c % 8 stored at slot
+  // (c % 8) ^ ((d / 2) % 8), which makes the 16-byte fragment reads of 16
+  // consecutive rows hit all 64 LDS banks once.  Out-of-range keys read a
+  // valid address and are zeroed by value.
   constexpr int KCH = D / 8;
   u32x4 rk[CPT], rv[CPT];
 
+  // Offsets are 32-bit element offsets from the per-head base pointers
+  // (a head's K is L * d elements, its V^T d * vt_ld: far below 2^31).
+  const int Li = (int)L;
+  const int vld = (int)vt_ld;
 #define ATTN_GLOAD(J0)                                                                  \
   do {                                                                                  \
     _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
       const int c_ = tid + 256 * i;                                                     \
-      const int64_t key_ = (J0) + c_ / KCH;                                             \
-      rk[i] = *reinterpret_cast<const u32x4*>(Kh + (key_ < L ? key_ : L - 1) * D +      \
-                                              (c_ % KCH) * 8);                          \
+      const int key_ = (J0) + c_ / KCH;                                                 \
+      const uint32_t off_ = (uint32_t)((key_ < Li ? key_ : Li - 1) * D + (c_ % KCH) * 8); \
+      rk[i] = *reinterpret_cast<const u32x4*>(Kh + off_);                               \
     }                                                                                   \
     _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
       const int c_ = tid + 256 * i;                                                     \
-      const int64_t key0_ = (J0) + (c_ & 7) * 8;                                        \
-      rv[i] = *reinterpret_cast<const u32x4*>(Vh + (int64_t)(c_ >> 3) * vt_ld +         \
-                                              (key0_ < L ? key0_ : 0));                 \
+      const int key0_ = (J0) + (c_ & 7) * 8;                                            \
+      const uint32_t off_ = (uint32_t)((c_ >> 3) * vld + (key0_ < Li ? key0_ : 0));     \
+      rv[i] = *reinterpret_cast<const u32x4*>(Vh + off_);                               \
     }                                                                                   \
   } while (0)
-// Masks keys >= L (by value) while writing the staged tile J0 to LDS.
+// Writes the staged tile J0 to LDS.  Only a tile that reaches past L (the
+// last one) needs masking: keys >= L are zeroed by value.
 #define ATTN_SSTORE(BUF, J0)                                                            \
   do {                                                                                  \
+    const bool tail_ = (J0) + BKV > Li;                                                 \
     _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
       const int c_ = tid + 256 * i;                                                     \
-      const uint32_t m_ = ((J0) + c_ / KCH < L) ? 0xFFFFFFFFu : 0u;                     \
-      *reinterpret_cast<u32x4*>(Ks + (BUF) * Ld::K_ELEMS + (c_ / KCH) * KLD +           \
-                                (c_ % KCH) * 8) = rk[i] & m_;                           \
-      const int64_t key0_ = (J0) + (c_ & 7) * 8;                                        \
-      const int64_t valid_ = key0_ < L ? L - key0_ : 0;                                 \
-      u32x4 vm_;                                                                        \
-      _Pragma("unroll") for (int p_ = 0; p_ < 4; ++p_)                                  \
-        vm_[p_] = ((2 * p_ < valid_) ? 0x0000FFFFu : 0u) |                              \
-                  ((2 * p_ + 1 < valid_) ? 0xFFFF0000u : 0u);                           \
+      u32x4 kv_ = rk[i], vv_ = rv[i];                                                   \
+      if (tail_) {                                                                      \
+        const uint32_t m_ = ((J0) + c_ / KCH < Li) ? 0xFFFFFFFFu : 0u;                  \
+        kv_ &= m_;                                                                      \
+        const int key0_ = (J0) + (c_ & 7) * 8;                                          \
+        const int valid_ = key0_ < Li ? Li - key0_ : 0;                                 \
+        u32x4 vm_;                                                                      \
+        _Pragma("unroll") for (int p_ = 0; p_ < 4; ++p_)                                \
+          vm_[p_] = ((2 * p_ < valid_) ? 0x0000FFFFu : 0u) |                            \
+                    ((2 * p_ + 1 < valid_) ? 0xFFFF0000u : 0u);                         \
+        vv_ &= vm_;                                                                     \
+      }                                                                                 \
+      *reinterpret_cast<u32x4*>(Ks + (BUF) * Ld::K_ELEMS + key_perm(c_ / KCH) * KLD +   \
+                                (c_ % KCH) * 8) = kv_;                                  \
       *reinterpret_cast<u32x4*>(Vs + (BUF) * Ld::V_ELEMS + (c_ >> 3) * VLD +            \
-                                (c_ & 7) * 8) = rv[i] & vm_;                            \
+                                (((c_ & 7) ^ ((c_ >> 4) & 7)) * 8)) = vv_;              \
     }                                                                                   \
   } while (0)
 
-  const int64_t nkv = (L + BKV - 1) / BKV;
+  const int nkv = (Li + BKV - 1) / BKV;
   ATTN_GLOAD(0);
   ATTN_SSTORE(0, 0);
   __syncthreads();
   // Unconditional prefetch (the last tile reloads itself into the idle
   // buffer): no branches around the staging registers.
-  for (int64_t it = 0; it < nkv; ++it) {
-    const int buf = (int)(it & 1);
-    const int64_t j0 = it * BKV;
-    const int64_t jn = (it + 1 < nkv ? it + 1 : it) * BKV;
+  for (int it = 0; it < nkv; ++it) {
+    const int buf = it & 1;
+    const int j0 = it * BKV;
+    const int jn = (it + 1 < nkv ? it + 1 : it) * BKV;
     ATTN_GLOAD(jn);
     asm volatile("" ::: "memory");     // no IR pass may sink the prefetch
     __builtin_amdgcn_sched_barrier(0);  // nor the machine scheduler
@@ -144,13 +181,14 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
       }
     }
     // Keys past L exist only in the last tile: mask them there (uniform branch).
-    if (j0 + BKV > L) {
+    if (j0 + BKV > Li) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int64_t key = j0 + kb * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
-          if (key >= L) s[kb][r] = -__builtin_inff();
+          // S^T row kb*32 + 8 (r/4) + 4 lg + r%4 holds key key_perm(row).
+          const int key = j0 + kb * 32 + 16 * (r >> 3) + 8 * lg + 4 * ((r >> 2) & 1) + (r & 3);
+          if (key >= Li) s[kb][r] = -__builtin_inff();
         }
     }
     // Row max of the raw scores (scale > 0 commutes with max), shared with
@@ -191,20 +229,18 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
     l_run += psum;
 
     // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
-    // (kb, k2) is key kb*32 + 16 k2 + 8 (e / 4) + 4 lg + e % 4, matching the
-    // accumulator rows of S^T that became pf[kb][k2].
+    // (kb, k2) is S^T row kb*32 + 16 k2 + 8 (e/4) + 4 lg + e%4, i.e. key
+    // kb*32 + 16 k2 + 8 lg + e: eight consecutive keys, one 16-byte chunk
+    // (4 kb + 2 k2 + lg) of the V^T row.
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
-      const bf16* vbase = Vs + buf * Ld::V_ELEMS + (db * 32 + lr) * VLD + 4 * lg;
+      const bf16* vrow = Vs + buf * Ld::V_ELEMS + (db * 32 + lr) * VLD;
+      const int sw = (lr >> 1) & 7;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int kb = ks >> 1, k2 = ks & 1;
-        const bf16* p = vbase + kb * 32 + k2 * 16;
-        bf16x4 lo = *reinterpret_cast<const bf16x4*>(p);
-        bf16x4 hi = *reinterpret_cast<const bf16x4*>(p + 8);
-        bf16x8 vf;
-        vf[0] = lo[0]; vf[1] = lo[1]; vf[2] = lo[2]; vf[3] = lo[3];
-        vf[4] = hi[0]; vf[5] = hi[1]; vf[6] = hi[2]; vf[7] = hi[3];
+        const bf16x8 vf =
+            *reinterpret_cast<const bf16x8*>(vrow + (((4 * kb + 2 * k2 + lg) ^ sw) * 8));
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][k2], o[db], 0, 0, 0);
       }
     }
@@ -311,7 +347,7 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
     attr_set = true;
   }
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
-  dim3 grid((unsigned)((L + BQ - 1) / BQ), (unsigned)n_heads);
+  dim3 grid((unsigned)(((L + BQ - 1) / BQ) * n_heads));
   hipLaunchKernelGGL(attn_bf16_kernel<D>, grid, dim3(256), AttnLds<D>::BYTES, s,
                      (const bf16*)q, (const bf16*)k, (const bf16*)vt, L, vt_ld, n_heads,
                      (bf16*)o, scale_log2);
