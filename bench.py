@@ -60,6 +60,21 @@ def work_per_class(cfg, n_computed: int, n_steps: int) -> dict:
     }
 
 
+def measured_traffic(kernel_source: str, record: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    record (rocprofv3 FETCH_SIZE / WRITE_SIZE passes scaled by the copy
+    calibration), or None if the kernel source changed since it was taken."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, record)))
+        sha = hashlib.sha256(open(os.path.join(ROOT, kernel_source), "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256") != sha:
+        return None
+    return rec["hbm_bytes_per_dispatch"]
+
+
 def cpu_baseline(ai, cfg, n_computed: int, n_steps: int, threads: int) -> dict:
     """The oracle on a bounded sample: one DiT block (full keys/values, R query
     rows at two values of R, extrapolated linearly to all rows), plus TEMNI,
@@ -217,8 +232,12 @@ def main() -> int:
         per_launch = 4.0 * L * L * H
         avg_s = kernels["attention"]["avg_us"] * 1e-6
         ach = per_launch / avg_s / 1e12
+        traffic = None
+        if cfg.head_dim == 128 and cfg.name == "wan2.1-1.3b-shape":
+            traffic = measured_traffic("paper_2607_12358_amd/csrc/attention.hip",
+                                       "profiles/attention_counters.json")
         roofline = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": ach / PEAK_BF16_TFLOPS, "traffic": None,
+                    "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic,
                     "kernel": "attn_bf16_kernel<128>", "flop_per_launch": per_launch,
                     "avg_launch_us": avg_s * 1e6}
 

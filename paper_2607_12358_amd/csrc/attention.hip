@@ -27,7 +27,7 @@ constexpr int BQ = 128, BKV = 64;
 
 template <int D>
 struct AttnLds {
-  static constexpr int KLD = D + 8;     // K tile row stride (elements), padded
+  static constexpr int KLD = D;         // K tile row stride (elements), XOR-swizzled
   static constexpr int VLD = BKV;       // V^T tile row stride: 128 B, XOR-swizzled
   static constexpr int K_ELEMS = BKV * KLD;
   static constexpr int V_ELEMS = D * VLD;
@@ -40,6 +40,31 @@ struct AttnLds {
 // 16-byte LDS read.
 __device__ __forceinline__ int key_perm(int j) {
   return (j & ~12) | ((j & 4) << 1) | ((j & 8) >> 1);
+}
+
+// 16-byte slot of chunk c in row r of a tile with 2^log2c chunks per row:
+// 16 consecutive rows read at one chunk cover all 64 four-byte LDS banks
+// (rows of 256 B start on the same bank: XOR with r % 16; rows of 128 B
+// alternate halves: XOR with (r / 2) % 8).
+template <int CHUNKS>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (CHUNKS == 16) return c ^ (r & 15);
+  else return c ^ ((r >> 1) & 7);
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One 16-byte-per-lane global -> LDS DMA: lane l writes LDS bytes
+// [lds + 16 l, +16).  Inline assembly keeps it out of the compiler's
+// wait-count bookkeeping (completion is waited for explicitly).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_byte) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(g), "s"(lds_byte)
+      : "memory");
 }
 
 // Bijection from dispatch order to (head, query-tile) work items that gives
@@ -99,19 +124,38 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -__builtin_inff(), l_run = 0.f;
 
-  // Staging: thread tid moves chunk c = tid + 256 i of each tile.  K tile:
-  // key c / (D/8) into row key_perm(key), chunk c % (D/8).  V^T tile: row
-  // c / 8 (a head dim d), 8-key chunk c % 8 stored at slot
-  // (c % 8) ^ ((d / 2) % 8), which makes the 16-byte fragment reads of 16
-  // consecutive rows hit all 64 LDS banks once.  Out-of-range keys read a
-  // valid address and are zeroed by value.
-  constexpr int KCH = D / 8;
+  // Staging.  Full tiles go global -> LDS by DMA: instruction i of wave w
+  // fills 1 KB at (4 w + i) KB of the tile (K: D/32 instructions per wave,
+  // V^T: D/32).  K tile: LDS row r (D * 2 bytes) holds key j0 + key_perm(r);
+  // V^T tile: LDS row d (128 bytes) holds keys j0 .. j0+63 of head dim d.
+  // Chunks sit at swizzled slots (swz).  The tail tile (the one reaching past
+  // L) is staged through registers instead, with keys >= L zeroed.
+  constexpr int KCH = D / 8;              // 16-byte chunks per K row
+  constexpr int KROWS_PER_KB = 1024 / (2 * D);  // K rows per 1 KB
   u32x4 rk[CPT], rv[CPT];
-
   // Offsets are 32-bit element offsets from the per-head base pointers
   // (a head's K is L * d elements, its V^T d * vt_ld: far below 2^31).
   const int Li = (int)L;
   const int vld = (int)vt_ld;
+  const uint32_t ks_lds = (uint32_t)(uintptr_t)(lds_void_t*)Ks;
+  const uint32_t vs_lds = (uint32_t)(uintptr_t)(lds_void_t*)Vs;
+#define ATTN_DMA(BUF, J0)                                                               \
+  do {                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
+      const int blk_ = wave * CPT + i;                                                  \
+      const int r_ = blk_ * KROWS_PER_KB + lane / KCH;                                  \
+      const int c_ = swz<KCH>(r_, lane % KCH);                                          \
+      dma16(Kh + (uint32_t)(((J0) + key_perm(r_)) * D + c_ * 8),                        \
+            __builtin_amdgcn_readfirstlane(ks_lds + ((BUF) * Ld::K_ELEMS) * 2 + blk_ * 1024)); \
+    }                                                                                   \
+    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
+      const int blk_ = wave * CPT + i;                                                  \
+      const int d_ = blk_ * 8 + (lane >> 3);                                            \
+      const int c_ = swz<8>(d_, lane & 7);                                              \
+      dma16(Vh + (uint32_t)(d_ * vld + (J0) + c_ * 8),                                  \
+            __builtin_amdgcn_readfirstlane(vs_lds + ((BUF) * Ld::V_ELEMS) * 2 + blk_ * 1024)); \
+    }                                                                                   \
+  } while (0)
 #define ATTN_GLOAD(J0)                                                                  \
   do {                                                                                  \
     _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
@@ -127,45 +171,50 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
       rv[i] = *reinterpret_cast<const u32x4*>(Vh + off_);                               \
     }                                                                                   \
   } while (0)
-// Writes the staged tile J0 to LDS.  Only a tile that reaches past L (the
-// last one) needs masking: keys >= L are zeroed by value.
+// Writes the register-staged tail tile J0 to LDS with keys >= L zeroed.
 #define ATTN_SSTORE(BUF, J0)                                                            \
   do {                                                                                  \
-    const bool tail_ = (J0) + BKV > Li;                                                 \
     _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
       const int c_ = tid + 256 * i;                                                     \
       u32x4 kv_ = rk[i], vv_ = rv[i];                                                   \
-      if (tail_) {                                                                      \
-        const uint32_t m_ = ((J0) + c_ / KCH < Li) ? 0xFFFFFFFFu : 0u;                  \
-        kv_ &= m_;                                                                      \
-        const int key0_ = (J0) + (c_ & 7) * 8;                                          \
-        const int valid_ = key0_ < Li ? Li - key0_ : 0;                                 \
-        u32x4 vm_;                                                                      \
-        _Pragma("unroll") for (int p_ = 0; p_ < 4; ++p_)                                \
-          vm_[p_] = ((2 * p_ < valid_) ? 0x0000FFFFu : 0u) |                            \
-                    ((2 * p_ + 1 < valid_) ? 0xFFFF0000u : 0u);                         \
-        vv_ &= vm_;                                                                     \
-      }                                                                                 \
-      *reinterpret_cast<u32x4*>(Ks + (BUF) * Ld::K_ELEMS + key_perm(c_ / KCH) * KLD +   \
-                                (c_ % KCH) * 8) = kv_;                                  \
+      kv_ &= ((J0) + c_ / KCH < Li) ? 0xFFFFFFFFu : 0u;                                 \
+      const int key0_ = (J0) + (c_ & 7) * 8;                                            \
+      const int valid_ = key0_ < Li ? Li - key0_ : 0;                                   \
+      u32x4 vm_;                                                                        \
+      _Pragma("unroll") for (int p_ = 0; p_ < 4; ++p_)                                  \
+        vm_[p_] = ((2 * p_ < valid_) ? 0x0000FFFFu : 0u) |                              \
+                  ((2 * p_ + 1 < valid_) ? 0xFFFF0000u : 0u);                           \
+      vv_ &= vm_;                                                                       \
+      const int kr_ = key_perm(c_ / KCH);                                               \
+      *reinterpret_cast<u32x4*>(Ks + (BUF) * Ld::K_ELEMS + kr_ * KLD +                  \
+                                swz<KCH>(kr_, c_ % KCH) * 8) = kv_;                     \
       *reinterpret_cast<u32x4*>(Vs + (BUF) * Ld::V_ELEMS + (c_ >> 3) * VLD +            \
-                                (((c_ & 7) ^ ((c_ >> 4) & 7)) * 8)) = vv_;              \
+                                swz<8>(c_ >> 3, c_ & 7) * 8) = vv_;                     \
     }                                                                                   \
+  } while (0)
+// Stages tile J0 (DMA, or registers for the tail) / completes it.
+#define ATTN_STAGE_BEGIN(BUF, J0)                                                       \
+  do {                                                                                  \
+    if ((J0) + BKV <= Li) ATTN_DMA(BUF, J0); else ATTN_GLOAD(J0);                       \
+  } while (0)
+#define ATTN_STAGE_END(BUF, J0)                                                         \
+  do {                                                                                  \
+    if ((J0) + BKV > Li) ATTN_SSTORE(BUF, J0);                                          \
+    __builtin_amdgcn_s_waitcnt(0);                                                      \
   } while (0)
 
   const int nkv = (Li + BKV - 1) / BKV;
-  ATTN_GLOAD(0);
-  ATTN_SSTORE(0, 0);
+  ATTN_STAGE_BEGIN(0, 0);
+  ATTN_STAGE_END(0, 0);
   __syncthreads();
-  // Unconditional prefetch (the last tile reloads itself into the idle
-  // buffer): no branches around the staging registers.
+  // The next tile streams in (DMA, or registers for the tail) while this one
+  // is consumed; past the last tile it reloads itself into the idle buffer.
   for (int it = 0; it < nkv; ++it) {
     const int buf = it & 1;
     const int j0 = it * BKV;
     const int jn = (it + 1 < nkv ? it + 1 : it) * BKV;
-    ATTN_GLOAD(jn);
-    asm volatile("" ::: "memory");     // no IR pass may sink the prefetch
-    __builtin_amdgcn_sched_barrier(0);  // nor the machine scheduler
+    ATTN_STAGE_BEGIN(buf ^ 1, jn);
+    __builtin_amdgcn_sched_barrier(0);
 
     // S^T (keys x queries) for two 32-key blocks.
     f32x16 s[2];
@@ -173,10 +222,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-      const bf16* kbase = Ks + buf * Ld::K_ELEMS + (kb * 32 + lr) * KLD + lg * 8;
+      const int kr = kb * 32 + lr;
+      const bf16* kbase = Ks + buf * Ld::K_ELEMS + kr * KLD;
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kbase + kk * 16);
+        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kbase + swz<KCH>(kr, 2 * kk + lg) * 8);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
       }
     }
@@ -235,21 +285,23 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
       const bf16* vrow = Vs + buf * Ld::V_ELEMS + (db * 32 + lr) * VLD;
-      const int sw = (lr >> 1) & 7;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int kb = ks >> 1, k2 = ks & 1;
-        const bf16x8 vf =
-            *reinterpret_cast<const bf16x8*>(vrow + (((4 * kb + 2 * k2 + lg) ^ sw) * 8));
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
+            vrow + swz<8>(db * 32 + lr, 4 * kb + 2 * k2 + lg) * 8);
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][k2], o[db], 0, 0, 0);
       }
     }
-    __builtin_amdgcn_sched_barrier(0);  // masks and LDS writes after the MFMAs
-    ATTN_SSTORE(buf ^ 1, jn);
+    __builtin_amdgcn_sched_barrier(0);  // tail writes and waits after the MFMAs
+    ATTN_STAGE_END(buf ^ 1, jn);
     __syncthreads();
   }
+#undef ATTN_DMA
 #undef ATTN_GLOAD
 #undef ATTN_SSTORE
+#undef ATTN_STAGE_BEGIN
+#undef ATTN_STAGE_END
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
