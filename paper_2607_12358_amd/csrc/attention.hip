@@ -1,20 +1,24 @@
 // Full non-causal multi-head self-attention over all video (and text) tokens.
 //
 // bf16 path: flash-style single pass on MFMA (v_mfma_f32_32x32x16_bf16).
-//   A workgroup owns 128 queries of one head (4 waves x 32 queries) and
-//   streams the head's keys in tiles of 64 through LDS, double-buffered with
-//   register prefetch.  Scores are formed transposed, S^T = K Q^T, so that a
-//   lane owns one query (lane % 32) and 16 keys per 32-key block: the row max
-//   is an in-register max plus one exchange with the partner half-wave, and
-//   the row sum stays a per-lane partial until the end.  The probabilities
-//   P^T in accumulator layout are exactly the B operand of O^T = V^T P^T when
-//   the contraction index is relabelled accordingly, so P never leaves
-//   registers; V is stored transposed (keys contiguous) by the QKV epilogue,
-//   and keys are staged into LDS in a permuted order so the matching A
-//   operand is one 16-byte read from an XOR-swizzled V^T tile (no LDS bank
-//   conflicts).  Work items are mapped so each XCD streams a contiguous,
-//   head-major range (a head's K/V passes through few L2s).  Softmax runs in the
-//   exp2 domain with log2(e)/sqrt(d) folded into one multiply, in fp32.
+//   A workgroup owns 32 queries per wave of one head (8 waves for d = 128,
+//   4 for d = 64) and streams the head's keys in tiles of 64 through two LDS
+//   ring buffers filled by global -> LDS DMA.  Scores are formed transposed,
+//   S^T = K Q^T, so that a lane owns one query (lane % 32) and 16 keys per
+//   32-key block: the row max is an in-register max plus one exchange with
+//   the partner half-wave (v_permlane32_swap), and the row sum stays a
+//   per-lane partial until the end.  The probabilities P^T in accumulator
+//   layout are exactly the B operand of O^T = V^T P^T when the contraction
+//   index is relabelled accordingly, so P never leaves registers; V is stored
+//   transposed (keys contiguous) by the QKV epilogue, and keys are staged
+//   into LDS in a permuted order so the matching A operand is one 16-byte
+//   read from an XOR-swizzled V^T tile (no LDS bank conflicts).  Each wave
+//   runs a two-stage software pipeline (exponentials of one tile under the
+//   score MFMAs of the next, the next tile's row max under the P V MFMAs).
+//   Work items are mapped so each XCD streams a contiguous, head-major range
+//   (a head's K/V passes through few L2s).  Softmax runs in the exp2 domain
+//   with log2(e)/sqrt(d) folded into one FMA per score, in fp32; the row sum
+//   adds the bf16-rounded probabilities that the P V product uses.
 // fp32 path: one thread per query with K/V tiles in LDS, online softmax in
 //   fp32 (for the fp32 configuration).
 #include "common.h"
@@ -23,7 +27,7 @@ namespace acid {
 
 namespace {
 
-constexpr int BQ = 128, BKV = 64;
+constexpr int BKV = 64;
 
 template <int D>
 struct AttnLds {
@@ -54,16 +58,23 @@ __device__ __forceinline__ int swz(int r, int c) {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// One 16-byte-per-lane global -> LDS DMA: lane l writes LDS bytes
-// [lds + 16 l, +16).  Inline assembly keeps it out of the compiler's
-// wait-count bookkeeping (completion is waited for explicitly).
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_byte) {
+// One 16-byte-per-lane global -> LDS DMA: lane l reads 16 bytes at
+// base + off_bytes(l) and writes LDS bytes [lds + 16 l, +16).  base and lds
+// are wave-uniform (scalar registers).  Inline assembly keeps it out of the
+// compiler's wait-count bookkeeping (completion is waited for explicitly).
+__device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ void dma16(uint64_t base, uint32_t off_bytes, uint32_t lds_byte) {
   asm volatile(
-      "s_mov_b32 m0, %1\n\t"
+      "s_mov_b32 m0, %2\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
+      "global_load_lds_dwordx4 %0, %1"
       :
-      : "v"(g), "s"(lds_byte)
+      : "v"(off_bytes), "s"(base), "s"(lds_byte)
       : "memory");
 }
 
@@ -77,18 +88,38 @@ __device__ __forceinline__ int64_t attn_xcd_remap(int64_t bid, int64_t T) {
   return (x < r) ? x * (q + 1) + local : r * (q + 1) + (x - r) * q + local;
 }
 
-template <int D>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
+// Maximum of a value over the two half-waves (lanes l and l ^ 32).
+__device__ __forceinline__ float half_swap_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Software pipeline, per wave and key tile j (LDS holds K_{j+1} and V_j):
+//   VALU: p = 2^(s_j - m) for tile j (scores formed one iteration earlier),
+//   MFMA: S_{j+1} = K_{j+1} Q^T, then O^T += V_j^T P_j^T,
+//   VALU: row max of S_{j+1} (under the P V MFMAs),
+// so the softmax of one tile overlaps the score MFMAs of the next.  K runs
+// one tile ahead of V in the two LDS ring buffers: iteration j streams
+// K_{j+2} and V_{j+1} in while K_{j+1} and V_j are read.  Softmax does not
+// depend on the order of the keys, so the ragged last tile (keys up to L)
+// is processed first, staged through registers and masked in the prologue;
+// every tile of the loop is full and arrives by DMA.
+template <int D, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* Q,
                                                            const bf16* Kp,
                                                            const bf16* Vt,
                                                            int64_t L, int64_t vt_ld, int n_heads,
                                                            bf16* __restrict__ O,
                                                            float scale_log2) {
   using Ld = AttnLds<D>;
+  constexpr int BQ = 32 * NW, NT = 64 * NW;  // queries / threads per workgroup
   constexpr int KLD = Ld::KLD, VLD = Ld::VLD;
   constexpr int NK = D / 16;     // MFMA K-steps over the head dim
   constexpr int ND = D / 32;     // 32-row blocks of O^T
-  constexpr int CPT = D / 32;    // 16-byte chunks per thread per tile
+  constexpr int CPT = D / (8 * NW);  // 16-byte chunks per thread per tile (K, and V^T)
+  constexpr int KCH = D / 8;     // 16-byte chunks per K row
+  constexpr int KROWS_PER_KB = 1024 / (2 * D);  // K rows per 1 KB
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   bf16* Ks = reinterpret_cast<bf16*>(smem);
   bf16* Vs = Ks + 2 * Ld::K_ELEMS;
@@ -97,7 +128,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
   const int64_t item = attn_xcd_remap(blockIdx.x, n_qt * n_heads);
   const int head = (int)(item / n_qt);
   const int64_t qt = item - (int64_t)head * n_qt;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 31, lg = lane >> 5;
   const int64_t qrow = qt * BQ + wave * 32 + lr;
 
@@ -124,184 +156,226 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(const bf16* Q,
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -__builtin_inff(), l_run = 0.f;
 
-  // Staging.  Full tiles go global -> LDS by DMA: instruction i of wave w
-  // fills 1 KB at (4 w + i) KB of the tile (K: D/32 instructions per wave,
-  // V^T: D/32).  K tile: LDS row r (D * 2 bytes) holds key j0 + key_perm(r);
-  // V^T tile: LDS row d (128 bytes) holds keys j0 .. j0+63 of head dim d.
-  // Chunks sit at swizzled slots (swz).  The tail tile (the one reaching past
-  // L) is staged through registers instead, with keys >= L zeroed.
-  constexpr int KCH = D / 8;              // 16-byte chunks per K row
-  constexpr int KROWS_PER_KB = 1024 / (2 * D);  // K rows per 1 KB
-  u32x4 rk[CPT], rv[CPT];
-  // Offsets are 32-bit element offsets from the per-head base pointers
-  // (a head's K is L * d elements, its V^T d * vt_ld: far below 2^31).
+  // Offsets are 32-bit (a head's K is L * d elements, its V^T d * vt_ld:
+  // far below 2^31 bytes).
   const int Li = (int)L;
   const int vld = (int)vt_ld;
   const uint32_t ks_lds = (uint32_t)(uintptr_t)(lds_void_t*)Ks;
   const uint32_t vs_lds = (uint32_t)(uintptr_t)(lds_void_t*)Vs;
-#define ATTN_DMA(BUF, J0)                                                               \
-  do {                                                                                  \
-    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
-      const int blk_ = wave * CPT + i;                                                  \
-      const int r_ = blk_ * KROWS_PER_KB + lane / KCH;                                  \
-      const int c_ = swz<KCH>(r_, lane % KCH);                                          \
-      dma16(Kh + (uint32_t)(((J0) + key_perm(r_)) * D + c_ * 8),                        \
-            __builtin_amdgcn_readfirstlane(ks_lds + ((BUF) * Ld::K_ELEMS) * 2 + blk_ * 1024)); \
-    }                                                                                   \
-    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
-      const int blk_ = wave * CPT + i;                                                  \
-      const int d_ = blk_ * 8 + (lane >> 3);                                            \
-      const int c_ = swz<8>(d_, lane & 7);                                              \
-      dma16(Vh + (uint32_t)(d_ * vld + (J0) + c_ * 8),                                  \
-            __builtin_amdgcn_readfirstlane(vs_lds + ((BUF) * Ld::V_ELEMS) * 2 + blk_ * 1024)); \
-    }                                                                                   \
-  } while (0)
-#define ATTN_GLOAD(J0)                                                                  \
-  do {                                                                                  \
-    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
-      const int c_ = tid + 256 * i;                                                     \
-      const int key_ = (J0) + c_ / KCH;                                                 \
-      const uint32_t off_ = (uint32_t)((key_ < Li ? key_ : Li - 1) * D + (c_ % KCH) * 8); \
-      rk[i] = *reinterpret_cast<const u32x4*>(Kh + off_);                               \
-    }                                                                                   \
-    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
-      const int c_ = tid + 256 * i;                                                     \
-      const int key0_ = (J0) + (c_ & 7) * 8;                                            \
-      const uint32_t off_ = (uint32_t)((c_ >> 3) * vld + (key0_ < Li ? key0_ : 0));     \
-      rv[i] = *reinterpret_cast<const u32x4*>(Vh + off_);                               \
-    }                                                                                   \
-  } while (0)
-// Writes the register-staged tail tile J0 to LDS with keys >= L zeroed.
-#define ATTN_SSTORE(BUF, J0)                                                            \
-  do {                                                                                  \
-    _Pragma("unroll") for (int i = 0; i < CPT; ++i) {                                   \
-      const int c_ = tid + 256 * i;                                                     \
-      u32x4 kv_ = rk[i], vv_ = rv[i];                                                   \
-      kv_ &= ((J0) + c_ / KCH < Li) ? 0xFFFFFFFFu : 0u;                                 \
-      const int key0_ = (J0) + (c_ & 7) * 8;                                            \
-      const int valid_ = key0_ < Li ? Li - key0_ : 0;                                   \
-      u32x4 vm_;                                                                        \
-      _Pragma("unroll") for (int p_ = 0; p_ < 4; ++p_)                                  \
-        vm_[p_] = ((2 * p_ < valid_) ? 0x0000FFFFu : 0u) |                              \
-                  ((2 * p_ + 1 < valid_) ? 0xFFFF0000u : 0u);                           \
-      vv_ &= vm_;                                                                       \
-      const int kr_ = key_perm(c_ / KCH);                                               \
-      *reinterpret_cast<u32x4*>(Ks + (BUF) * Ld::K_ELEMS + kr_ * KLD +                  \
-                                swz<KCH>(kr_, c_ % KCH) * 8) = kv_;                     \
-      *reinterpret_cast<u32x4*>(Vs + (BUF) * Ld::V_ELEMS + (c_ >> 3) * VLD +            \
-                                swz<8>(c_ >> 3, c_ & 7) * 8) = vv_;                     \
-    }                                                                                   \
-  } while (0)
-// Stages tile J0 (DMA, or registers for the tail) / completes it.
-#define ATTN_STAGE_BEGIN(BUF, J0)                                                       \
-  do {                                                                                  \
-    if ((J0) + BKV <= Li) ATTN_DMA(BUF, J0); else ATTN_GLOAD(J0);                       \
-  } while (0)
-#define ATTN_STAGE_END(BUF, J0)                                                         \
-  do {                                                                                  \
-    if ((J0) + BKV > Li) ATTN_SSTORE(BUF, J0);                                          \
-    __builtin_amdgcn_s_waitcnt(0);                                                      \
-  } while (0)
 
-  const int nkv = (Li + BKV - 1) / BKV;
-  ATTN_STAGE_BEGIN(0, 0);
-  ATTN_STAGE_END(0, 0);
-  __syncthreads();
-  // The next tile streams in (DMA, or registers for the tail) while this one
-  // is consumed; past the last tile it reloads itself into the idle buffer.
-  for (int it = 0; it < nkv; ++it) {
-    const int buf = it & 1;
-    const int j0 = it * BKV;
-    const int jn = (it + 1 < nkv ? it + 1 : it) * BKV;
-    ATTN_STAGE_BEGIN(buf ^ 1, jn);
-    __builtin_amdgcn_sched_barrier(0);
-
-    // S^T (keys x queries) for two 32-key blocks.
-    f32x16 s[2];
+  // DMA staging of a full tile: instruction i of wave w fills 1 KB at
+  // (CPT w + i) KB of the tile.  K tile: LDS row r (D * 2 bytes) holds key
+  // j0 + key_perm(r); V^T tile: LDS row d (128 bytes) holds keys j0 .. j0+63
+  // of head dim d; chunks sit at swizzled slots (swz).  Per-lane byte offsets
+  // relative to the tile's first element:
+  uint32_t koff[CPT], voff[CPT];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+  for (int i = 0; i < CPT; ++i) {
+    const int blk = wave * CPT + i;
+    const int r = blk * KROWS_PER_KB + lane / KCH;
+    koff[i] = (uint32_t)(key_perm(r) * D + swz<KCH>(r, lane % KCH) * 8) * 2u;
+    const int d = blk * 8 + (lane >> 3);
+    voff[i] = (uint32_t)(d * vld + swz<8>(d, lane & 7) * 8) * 2u;
+  }
+  auto stage_k_dma = [&](int buf, int j0) {
+    const uint64_t base = uniform_ptr(Kh + (int64_t)j0 * D);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      dma16(base, koff[i], ks_lds + buf * Ld::K_ELEMS * 2 + (wave * CPT + i) * 1024);
+  };
+  auto stage_v_dma = [&](int buf, int j0) {
+    const uint64_t base = uniform_ptr(Vh + j0);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      dma16(base, voff[i], vs_lds + buf * Ld::V_ELEMS * 2 + (wave * CPT + i) * 1024);
+  };
+  // The ragged tile j0 .. L-1 through registers, keys >= L zeroed (K rows,
+  // and V^T columns, whose padding past L may hold anything).
+  auto stage_tail = [&](int buf, int j0) {
+    u32x4 rk[CPT], rv[CPT];
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + NT * i;
+      const int key = j0 + c / KCH;
+      rk[i] = *reinterpret_cast<const u32x4*>(
+          Kh + (uint32_t)((key < Li ? key : Li - 1) * D + (c % KCH) * 8));
+      const int key0 = j0 + (c & 7) * 8;
+      rv[i] = *reinterpret_cast<const u32x4*>(Vh + (uint32_t)((c >> 3) * vld +
+                                                              (key0 < Li ? key0 : 0)));
+    }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + NT * i;
+      u32x4 kv = rk[i];
+      kv &= (j0 + c / KCH < Li) ? 0xFFFFFFFFu : 0u;
+      const int kr = key_perm(c / KCH);
+      *reinterpret_cast<u32x4*>(Ks + buf * Ld::K_ELEMS + kr * KLD + swz<KCH>(kr, c % KCH) * 8) =
+          kv;
+      const int key0 = j0 + (c & 7) * 8;
+      const int valid = key0 < Li ? Li - key0 : 0;
+      u32x4 vm;
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        vm[p] = ((2 * p < valid) ? 0x0000FFFFu : 0u) | ((2 * p + 1 < valid) ? 0xFFFF0000u : 0u);
+      *reinterpret_cast<u32x4*>(Vs + buf * Ld::V_ELEMS + (c >> 3) * VLD +
+                                swz<8>(c >> 3, c & 7) * 8) = rv[i] & vm;
+    }
+  };
+
+  // S^T (keys x queries) of the K tile in buffer kbuf, two 32-key blocks.
+  auto scores = [&](f32x16(&s)[2], int kbuf) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-      const int kr = kb * 32 + lr;
-      const bf16* kbase = Ks + buf * Ld::K_ELEMS + kr * KLD;
 #pragma unroll
-      for (int kk = 0; kk < NK; ++kk) {
-        bf16x8 kf = *reinterpret_cast<const bf16x8*>(kbase + swz<KCH>(kr, 2 * kk + lg) * 8);
+    for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int kr = kb * 32 + lr;
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + kbuf * Ld::K_ELEMS + kr * KLD +
+                                                            swz<KCH>(kr, 2 * kk + lg) * 8);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
       }
-    }
-    // Keys past L exist only in the last tile: mask them there (uniform branch).
-    if (j0 + BKV > Li) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          // S^T row kb*32 + 8 (r/4) + 4 lg + r%4 holds key key_perm(row).
-          const int key = j0 + kb * 32 + 16 * (r >> 3) + 8 * lg + 4 * ((r >> 2) & 1) + (r & 3);
-          if (key >= Li) s[kb][r] = -__builtin_inff();
-        }
-    }
-    // Row max of the raw scores (scale > 0 commutes with max), shared with
-    // the partner half-wave that holds the other keys of the same query.
+  };
+  // Row max of a raw score tile (scale > 0 commutes with max), shared with
+  // the partner half-wave that holds the other keys of the same query, then
+  // the tile is rewritten in place as s log2(e)/sqrt(d) - m (exp2 argument).
+  // Lazy rescaling: the reference max m moves only when the new max exceeds
+  // it by more than 2^8 in probability, so probabilities stay <= 256 (exact
+  // range for bf16 and fp32) and the O / l rescale is skipped on most tiles.
+  float m_nx, a_nx;
+  bool g_nx;
+  auto row_max_shift = [&](f32x16(&s)[2]) {
     float mx = s[0][0];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    // Lazy rescaling: the running reference max moves only when the new
-    // max exceeds it by more than 2^8 in probability, so probabilities stay
-    // <= 256 (exact range for bf16 and fp32) and the O / l rescale is skipped
-    // on most tiles.  The branch is wave-uniform.
+    mx = half_swap_max(mx);
     const float m_cand = mx * scale_log2;
-    const bool grow = m_cand > m_run + 8.0f;
-    if (__any(grow)) {
-      const float m_new = grow ? m_cand : m_run;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      m_run = m_new;
-      l_run *= alpha;
+    g_nx = m_cand > m_run + 8.0f;
+    m_nx = g_nx ? m_cand : m_run;
+    a_nx = __builtin_amdgcn_exp2f(m_run - m_nx);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = __builtin_fmaf(s[kb][r], scale_log2, -m_nx);
+  };
+  // p = 2^(shifted score), rounded to bf16 as the B operand of the P V
+  // MFMAs; the row sum adds exactly those bf16 values (v_dot2 with (1, 1)).
+  auto probs = [&](const f32x16(&s)[2], bf16x8(&pf)[2][2]) {
+    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+    float ps[2] = {0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = 8 * k2 + 2 * e;
+          const bf16x2 pr = {(bf16)__builtin_amdgcn_exp2f(s[kb][r]),
+                             (bf16)__builtin_amdgcn_exp2f(s[kb][r + 1])};
+          ps[e & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps[e & 1], false);
+          w[e] = __builtin_bit_cast(uint32_t, pr);
+        }
+        pf[kb][k2] = __builtin_bit_cast(bf16x8, w);
+      }
+    l_run += ps[0] + ps[1];
+  };
+  // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
+  // (kb, k2) is S^T row kb*32 + 16 k2 + 8 (e/4) + 4 lg + e%4, i.e. key
+  // kb*32 + 16 k2 + 8 lg + e: eight consecutive keys, one 16-byte chunk
+  // (4 kb + 2 k2 + lg) of the V^T row.
+  auto pv = [&](const bf16x8(&pf)[2][2], int vbuf) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int db = 0; db < ND; ++db) {
+        const int kb = ks >> 1, k2 = ks & 1;
+        const int vr = db * 32 + lr;
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(Vs + vbuf * Ld::V_ELEMS + vr * VLD +
+                                                            swz<8>(vr, 4 * kb + 2 * k2 + lg) * 8);
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][k2], o[db], 0, 0, 0);
+      }
+  };
+
+  // Processing order of the key tiles: the ragged tile (if any) first, then
+  // the full tiles in order.  u >= 1 maps to the full tile u - has_tail.
+  const int nkv = (Li + BKV - 1) / BKV;
+  const int has_tail = (Li % BKV) != 0;
+  // One pipeline iteration: sc holds S of processed tile it; S of tile it+1
+  // goes to sn (on the last tile this reads a stale buffer and is dropped).
+  auto iter = [&](f32x16(&sc)[2], f32x16(&sn)[2], int it) {
+    if (it + 2 < nkv) stage_k_dma(it & 1, (it + 2 - has_tail) * BKV);
+    if (it + 1 < nkv) stage_v_dma((it + 1) & 1, (it + 1 - has_tail) * BKV);
+    __builtin_amdgcn_sched_barrier(0);
+    m_run = m_nx;
+    if (__any(g_nx)) {
+      l_run *= a_nx;
 #pragma unroll
       for (int db = 0; db < ND; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        for (int r = 0; r < 16; ++r) o[db][r] *= a_nx;
     }
-    // p = 2^(s log2(e)/sqrt(d) - m): one FMA and one v_exp_f32 per score.
-    float psum = 0.f;
+    __builtin_amdgcn_sched_barrier(0);
     bf16x8 pf[2][2];
+    probs(sc, pf);
+    scores(sn, (it + 1) & 1);
+    pv(pf, it & 1);
+    row_max_shift(sn);
+    // Interleave: each score MFMA with one fragment read and a share of the
+    // exponentials, then each P V MFMA with one read and a share of the row
+    // max and shift of the next tile.
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int i = 0; i < 2 * NK; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, (66 + 2 * NK - 1) / (2 * NK), 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 4 * ND; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, (56 + 4 * ND - 1) / (4 * ND), 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);  // this iteration's staging has landed
+    __builtin_amdgcn_s_barrier();
+  };
+
+  f32x16 sa[2], sb[2];
+  if (has_tail) {
+    stage_tail(0, (nkv - 1) * BKV);
+  } else {
+    stage_k_dma(0, 0);
+    stage_v_dma(0, 0);
+  }
+  if (nkv > 1) stage_k_dma(1, (1 - has_tail) * BKV);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  scores(sa, 0);
+  if (has_tail) {
+    // Keys past L get score -inf.  S^T row kb*32 + 8 (r/4) + 4 lg + r%4
+    // holds key j0 + key_perm(row).
+    const int j0 = (nkv - 1) * BKV;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][r], scale_log2, -m_run));
-        psum += p;
-        pf[kb][r >> 3][r & 7] = (bf16)p;
+        const int key = j0 + kb * 32 + 16 * (r >> 3) + 8 * lg + 4 * ((r >> 2) & 1) + (r & 3);
+        if (key >= Li) sa[kb][r] = -__builtin_inff();
       }
-    l_run += psum;
-
-    // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
-    // (kb, k2) is S^T row kb*32 + 16 k2 + 8 (e/4) + 4 lg + e%4, i.e. key
-    // kb*32 + 16 k2 + 8 lg + e: eight consecutive keys, one 16-byte chunk
-    // (4 kb + 2 k2 + lg) of the V^T row.
-#pragma unroll
-    for (int db = 0; db < ND; ++db) {
-      const bf16* vrow = Vs + buf * Ld::V_ELEMS + (db * 32 + lr) * VLD;
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int kb = ks >> 1, k2 = ks & 1;
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(
-            vrow + swz<8>(db * 32 + lr, 4 * kb + 2 * k2 + lg) * 8);
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[kb][k2], o[db], 0, 0, 0);
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);  // tail writes and waits after the MFMAs
-    ATTN_STAGE_END(buf ^ 1, jn);
-    __syncthreads();
   }
-#undef ATTN_DMA
-#undef ATTN_GLOAD
-#undef ATTN_SSTORE
-#undef ATTN_STAGE_BEGIN
-#undef ATTN_STAGE_END
+  row_max_shift(sa);
+  int it = 0;
+  for (; it + 1 < nkv; it += 2) {
+    iter(sa, sb, it);
+    iter(sb, sa, it + 1);
+  }
+  if (it < nkv) iter(sa, sb, it);
 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
@@ -387,12 +461,16 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   }
 }
 
+// Waves per workgroup: 8 for d = 128 (a staged K/V tile feeds 256 queries),
+// 4 for d = 64 (finer grid for the shorter sequences of that configuration).
 template <int D>
 hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
                        int64_t vt_ld, void* o, hipStream_t s) {
+  constexpr int NW = D == 128 ? 8 : 4;
+  constexpr int BQ = 32 * NW;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute((const void*)attn_bf16_kernel<D>,
+    hipError_t err = hipFuncSetAttribute((const void*)attn_bf16_kernel<D, NW>,
                                          hipFuncAttributeMaxDynamicSharedMemorySize,
                                          (int)AttnLds<D>::BYTES);
     if (err != hipSuccess) return err;
@@ -400,7 +478,7 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
   }
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
   dim3 grid((unsigned)(((L + BQ - 1) / BQ) * n_heads));
-  hipLaunchKernelGGL(attn_bf16_kernel<D>, grid, dim3(256), AttnLds<D>::BYTES, s,
+  hipLaunchKernelGGL((attn_bf16_kernel<D, NW>), grid, dim3(64 * NW), AttnLds<D>::BYTES, s,
                      (const bf16*)q, (const bf16*)k, (const bf16*)vt, L, vt_ld, n_heads,
                      (bf16*)o, scale_log2);
   return hipGetLastError();
