@@ -2,22 +2,25 @@
 // needs (plain, tanh-GELU, gated residual add, QKV head split, Euler update).
 //
 // bf16 path: MFMA v_mfma_f32_32x32x16_bf16 (gfx950), fp32 accumulate.
-//   Macro tile 256 (tokens) x 256 (features), K in steps of 64, 4 waves in a
-//   2x2 grid, each wave 128 x 128 = 4 x 4 MFMA blocks of 32 x 32
-//   (accumulators in AGPRs).  Operands go global -> LDS directly
-//   (global_load_lds_dwordx4, no staging registers) into two 64 KB stages,
-//   K-contiguous 128-byte rows (whole cache lines, so the L2 request rate
-//   stays within budget) with an XOR swizzle that is conflict-free for
-//   gfx950's 64 LDS banks.  One barrier per K-step, placed before the last
-//   16-wide sub-step so the refill DMA and the next stage's first fragment
-//   reads hide behind its MFMAs; all other fragment reads are
-//   software-pipelined one sub-step ahead.  A 256 x 256 tile halves the
-//   operand bytes per flop of a 256 x 128 tile.  The activation tile feeds MFMA operand A
-//   and the weight tile operand B, so the accumulator holds C with lanes
-//   along features: every epilogue store is a run of consecutive features of
-//   one token row (coalesced), and bias / gate are one value per lane.
-//   Workgroups are remapped so each XCD (8 per MI355X, own L2) works on a
-//   contiguous group of tiles that share activation rows.
+//   Macro tile 256 (tokens) x 256 (features), K in steps of 64, 8 waves in a
+//   2 x 4 grid (two per SIMD), each wave 128 x 64 = 4 x 2 MFMA blocks of
+//   32 x 32.  Operands go global -> LDS directly (global_load_lds_dwordx4,
+//   no staging registers) into two 64 KB stages, K-contiguous 128-byte rows
+//   (whole cache lines, so the L2 request rate stays within budget) with an
+//   XOR swizzle that is conflict-free for gfx950's 64 LDS banks.  One
+//   barrier per K-step, placed before the last 16-wide sub-step so the
+//   refill DMA and the next stage's first fragment reads hide behind its
+//   MFMAs; all other fragment reads are software-pipelined one sub-step
+//   ahead.  A wave that issues global loads holds back its own MFMA issue,
+//   so two waves share each SIMD: one keeps the MFMA unit busy while the
+//   other issues its DMAs.  A 256 x 256 tile halves the operand bytes per
+//   flop of a 256 x 128 tile (operand traffic also costs clock under the
+//   power cap).  The activation tile feeds MFMA operand A and the weight
+//   tile operand B, so the accumulator holds C with lanes along features:
+//   every epilogue store is a run of consecutive features of one token row
+//   (coalesced), and bias / gate are one value per lane.  Workgroups are
+//   remapped so each XCD (8 per MI355X, own L2) works on a contiguous group
+//   of tiles that share activation rows.
 // fp32 path: a plain 64 x 64 register-blocked VALU kernel for the fp32
 //   configuration (small shapes, latency-bound).
 #include "common.h"
@@ -166,68 +169,50 @@ __device__ __forceinline__ void tile_coords(int64_t t, int64_t tiles_m, int tile
 // ------------------------------------------------------------ bf16 MFMA
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
 
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int kTileElems = 256 * BK;  // one operand tile per stage (32 KB)
+constexpr int kWaves = 8;                // 2 (tokens) x 4 (features), two per SIMD
+constexpr int kTileElems = 256 * BK;     // one operand tile per stage (32 KB)
 
-// One 256 x 64 operand tile (rows K-contiguous, 128 B = 8 chunks of 16 B per
-// row; every row fetch is one whole 128-byte line, which halves the L2
-// request rate of narrower K-steps) moved global -> LDS with
-// global_load_lds_dwordx4.  Instruction i of wave w fills LDS bytes
-// [(8 w + i) KB, +1 KB) = rows 64 w + 8 i .. +7; lane l lands in row
-// 64 w + 8 i + l / 8, slot l % 8, which holds global chunk
-// (l % 8) ^ ((row / 2) % 8).  With 64 four-byte LDS banks a row spans half
-// the banks, so 16 consecutive fragment rows read at one chunk cover all 64
-// banks exactly once.
+// One 16-byte-per-lane LDS-DMA: lane l reads 16 bytes at base + off(l) and
+// writes LDS bytes [lds + 16 l, +16).  base and lds are wave-uniform.
 // Issued as inline assembly so the compiler's wait-count pass does not see
-// the LDS-DMA (it cannot order DMA completions against LDS reads and would
-// drain every read).  Completion is tracked explicitly with vmcnt waits; M0
-// (the DMA's LDS base) is set here and the compiler issues no other M0 user
-// in this kernel.
-__device__ __forceinline__ void load_tile_lds(bf16* lds_tile, const bf16* const (&row_ptr)[8],
-                                              int chunk_even, int chunk_odd, int k0, int wave) {
-  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(lds_void_t*)(lds_tile + (wave * 8) * 512));
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const bf16* g = row_ptr[i] + k0 + ((i & 1) ? chunk_odd : chunk_even) * 8;
-    asm volatile(
-        "s_mov_b32 m0, %1\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %0, off"
-        :
-        : "v"(g), "s"(lds0 + i * 1024)
-        : "memory");
-  }
-}
-
-// One 16-byte-per-lane LDS-DMA (see load_tile_lds).
-__device__ __forceinline__ void dma16(const bf16* g, uint32_t lds_byte) {
+// it (that pass cannot order DMA completions against LDS reads and would
+// drain every read); completion is waited for explicitly.  M0 (the DMA's
+// LDS base) is set here and nothing else in these kernels uses M0.
+__device__ __forceinline__ void dma16(uint64_t base, uint32_t off_bytes, uint32_t lds_byte) {
   asm volatile(
-      "s_mov_b32 m0, %1\n\t"
+      "s_mov_b32 m0, %2\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
+      "global_load_lds_dwordx4 %0, %1"
       :
-      : "v"(g), "s"(lds_byte)
+      : "v"(off_bytes), "s"(base), "s"(lds_byte)
       : "memory");
 }
-
-// Waits until at most N of this wave's global loads are outstanding.  The
-// main loop pairs it with a bare s_barrier (no fence: __syncthreads would
-// also drain every in-flight prefetch): a wave's own LDS-DMA writes are
-// complete after the wait, everyone's after the barrier.
-// gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+__device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
 }
 __device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
 
+// Operand tiles are 256 rows x 64 (K-contiguous 128-byte rows: every row
+// fetch is one whole line).  DMA instruction i (0..3) of wave w fills LDS
+// bytes [(4 w + i) KB, +1 KB) = rows 32 w + 8 i .. +7; lane l lands in row
+// 32 w + 8 i + l / 8, slot l % 8, which holds global chunk
+// (l % 8) ^ ((row / 2) % 8) (= (l % 8) ^ (l / 16) for even i, ^ 4 more for
+// odd i).  With 64 four-byte LDS banks a row spans half the banks, so 16
+// consecutive fragment rows read at one chunk cover all 64 banks once.
+//
+// Eight waves, two per SIMD: while one wave of a SIMD stalls issuing its
+// DMAs (a wave that issues global loads holds back its own MFMA issue), the
+// other keeps the MFMA unit busy.  Each wave owns 128 x 64 of the tile
+// (4 x 2 blocks of 32 x 32, 128 accumulator registers).
 template <int KIND>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* A, const bf16* Wt,
-                                                           int64_t M, int N, int K, Epi e) {
+__global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A, const bf16* Wt,
+                                                                   int64_t M, int N, int K,
+                                                                   Epi e) {
   // Two stages of A and B tiles, one LDS object per tile so the compiler can
   // tell the stage being read from the stage being filled.
   __shared__ __attribute__((aligned(1024))) bf16 As0[kTileElems], Bs0[kTileElems];
@@ -241,103 +226,104 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* A, const 
   const int64_t m0 = tm * BM;
   const int n0 = tn * BN;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
   const int lr = lane & 31, lg = lane >> 5;
-  // A tile of width 128 at the right edge (N % 256 == 128): waves with wn = 1
-  // compute on clamped rows and store nothing.
-  const bool active = n0 + wn * 128 < N;
+  // A tile of width 128 at the right edge (N % 256 == 128): waves with
+  // wn >= 2 compute on clamped rows and store nothing.
+  const bool active = n0 + wn * 64 < N;
 
-  // Load-side addressing (rows past the edge are clamped: they only feed
-  // outputs that are never stored).
+  // Load-side addressing: byte offsets from the tile's first row (rows past
+  // the edge are clamped; they only feed outputs that are never stored).
   const int chunk_even = (lane & 7) ^ (lane >> 4);
   const int chunk_odd = (lane & 7) ^ ((lane >> 4) ^ 4);
-  const bf16* a_row[8];
-  const bf16* b_row[8];
+  const uint64_t a_base = uniform_ptr(A + m0 * K);
+  const uint64_t b_base = uniform_ptr(Wt + (int64_t)n0 * K);
+  uint32_t a_off[4], b_off[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int r = wave * 64 + i * 8 + (lane >> 3);
-    const int64_t gm = m0 + r < M ? m0 + r : M - 1;
-    const int gn = n0 + r < N ? n0 + r : N - 1;
-    a_row[i] = A + gm * K;
-    b_row[i] = Wt + (int64_t)gn * K;
+  for (int i = 0; i < 4; ++i) {
+    const int r = wave * 32 + i * 8 + (lane >> 3);
+    const int ra = m0 + r < M ? r : (int)(M - 1 - m0);
+    const int rb = n0 + r < N ? r : N - 1 - n0;
+    const int ch = (i & 1) ? chunk_odd : chunk_even;
+    a_off[i] = (uint32_t)(ra * K + ch * 8) * 2u;
+    b_off[i] = (uint32_t)(rb * K + ch * 8) * 2u;
   }
+  const uint32_t lds_wave = (uint32_t)(wave * 4 * 1024);
+  auto lds_addr = [&](const bf16* tile) {
+    return (uint32_t)(uintptr_t)(lds_void_t*)tile + lds_wave;
+  };
 
   // Read-side addressing: fragment row rr at K-step kk (16 wide) reads chunk
   // 2 kk + lg, stored at slot (2 kk + lg) ^ ((rr / 2) % 8), and
   // (rr / 2) % 8 == (lr / 2) % 8 for every fragment row of this lane.
-  const int a_base = (wm * 128 + lr) * BK;
-  const int b_base = (wn * 128 + lr) * BK;
+  const int a_rbase = (wm * 128 + lr) * BK;
+  const int b_rbase = (wn * 64 + lr) * BK;
   int sl[4];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) sl[kk] = 8 * ((2 * kk + lg) ^ ((lr >> 1) & 7));
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
-  auto read_frags = [&](const bf16* As, const bf16* Bs, int slot, bf16x8 (&fa)[4],
-                        bf16x8 (&fb)[4]) {
+  bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
+  auto read_frags = [&](const bf16* As, const bf16* Bs, int slot, bf16x8(&fa)[4],
+                        bf16x8(&fb)[2]) {
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
-      fa[mb] = *reinterpret_cast<const bf16x8*>(As + a_base + mb * 32 * BK + slot);
+      fa[mb] = *reinterpret_cast<const bf16x8*>(As + a_rbase + mb * 32 * BK + slot);
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-      fb[nb] = *reinterpret_cast<const bf16x8*>(Bs + b_base + nb * 32 * BK + slot);
+    for (int nb = 0; nb < 2; ++nb)
+      fb[nb] = *reinterpret_cast<const bf16x8*>(Bs + b_rbase + nb * 32 * BK + slot);
   };
-  auto mma = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4]) {
+  auto mma = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2]) {
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < 4; ++nb)
+      for (int nb = 0; nb < 2; ++nb)
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+  };
+  auto load_stage = [&](const bf16* As, const bf16* Bs, int k0) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(a_base, a_off[i] + k0 * 2, la + i * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(b_base, b_off[i] + k0 * 2, lb + i * 1024);
+  };
+  // The last K-step of a stage with the refill of its buffer interleaved:
+  // one DMA after each of the 8 MFMAs (order pinned by scheduling barriers).
+  auto mma_refill = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2], const bf16* As,
+                        const bf16* Bs, int kn) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+        const int j = mb * 2 + nb, i = j & 3;
+        if (j < 4)
+          dma16(a_base, a_off[i] + kn * 2, la + i * 1024);
+        else
+          dma16(b_base, b_off[i] + kn * 2, lb + i * 1024);
+        __builtin_amdgcn_sched_barrier(0);
+      }
   };
 
   const int KT = K / BK;  // even: K % 128 == 0
   // Prologue: stages 0 and 1 in flight, stage 0 landed, first fragments read.
-  load_tile_lds(As0, a_row, chunk_even, chunk_odd, 0, wave);
-  load_tile_lds(Bs0, b_row, chunk_even, chunk_odd, 0, wave);
-  load_tile_lds(As1, a_row, chunk_even, chunk_odd, BK, wave);
-  load_tile_lds(Bs1, b_row, chunk_even, chunk_odd, BK, wave);
-  wait_vmcnt<16>();
+  load_stage(As0, Bs0, 0);
+  load_stage(As1, Bs1, BK);
+  __builtin_amdgcn_s_waitcnt((8 & 15) | (7 << 4) | (15 << 8));  // vmcnt(8): stage 0 landed
   __builtin_amdgcn_s_barrier();
   read_frags(As0, Bs0, sl[0], fa0, fb0);
-
-  // Stage kt (buffer kt % 2): K-steps 0..2 with the next step's fragments
-  // read behind each MFMA group; then this wave's reads of the buffer are
-  // done and stage kt+1 has landed (waits), barrier (everyone's are),
-  // refill this buffer with stage kt+2 and read stage kt+1's first
-  // fragments, both hidden behind K-step 3's MFMAs.  Past the last stage the
-  // refill reloads stage KT-1 into a buffer that is never read again.
-  // The refill of one stage is 16 DMA instructions per wave (8 for A, 8 for
-  // B).  Issuing them back to back stalls the wave on the memory pipe while
-  // the MFMA unit idles, so they are interleaved one per MFMA of the last
-  // sub-step (ordering pinned with scheduling barriers).
-  auto mma_refill = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4], bf16* As, bf16* Bs,
-                        int kn) {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)(lds_void_t*)(As + (wave * 8) * 512));
-    const uint32_t lb = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)(lds_void_t*)(Bs + (wave * 8) * 512));
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < 4; ++nb) {
-        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
-        const int j = mb * 4 + nb, i = j & 7;
-        const int ch = (i & 1) ? chunk_odd : chunk_even;
-        if (j < 8)
-          dma16(a_row[i] + kn + ch * 8, la + i * 1024);
-        else
-          dma16(b_row[i] + kn + ch * 8, lb + i * 1024);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-  };
 
   // Stage kt (buffer kt % 2): K-steps 0..2 with the next step's fragments
   // read behind each MFMA group; then this wave's reads of the buffer are
@@ -373,32 +359,37 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const bf16* A, const 
     --kt;
   }
 #undef GEMM_STAGE
+  wait_all();  // the last refill lands before the workgroup's LDS is released
   if (!active) return;
 
   // D[i][j] of a 32x32 block: j = lane % 32, i = 8 (r / 4) + 4 (lane / 32) + r % 4.
   // A lane owns one feature column per 32-wide block: set up its epilogue
   // once, then handle its 64 rows of that column.  Full tiles skip the row
   // check (a per-element branch would serialise every load behind a wait);
-  // read-modify-write kinds issue all 64 loads before any store.
+  // read-modify-write kinds issue 32 loads before their stores.
   const bool full = m0 + BM <= M;
   const int64_t mrow = m0 + wm * 128 + 4 * lg;
 #pragma unroll
-  for (int nb = 0; nb < 4; ++nb) {
-    const int n = n0 + wn * 128 + nb * 32 + lr;
+  for (int nb = 0; nb < 2; ++nb) {
+    const int n = n0 + wn * 64 + nb * 32 + lr;
     ColEpi<KIND, bf16> ce(e, n, N);
     if (full) {
       if constexpr (ColEpi<KIND, bf16>::kRmw) {
-        float prev[4][16];
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
+        for (int h = 0; h < 2; ++h) {  // 32 loads in flight, then 32 stores
+          float prev[2][16];
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            prev[mb][r] = ce.old(mrow + mb * 32 + 8 * (r >> 2) + (r & 3));
+          for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
+            for (int r = 0; r < 16; ++r)
+              prev[mb][r] = ce.old(mrow + (2 * h + mb) * 32 + 8 * (r >> 2) + (r & 3));
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            ce.put_old(mrow + mb * 32 + 8 * (r >> 2) + (r & 3), acc[mb][nb][r], prev[mb][r]);
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              ce.put_old(mrow + (2 * h + mb) * 32 + 8 * (r >> 2) + (r & 3),
+                         acc[2 * h + mb][nb][r], prev[mb][r]);
+        }
       } else {
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb)
@@ -472,7 +463,7 @@ hipError_t launch_kind(int dtype, int64_t M, int N, int K, const void* a, const 
                        const Epi& e, hipStream_t s) {
   if (dtype == ACID_BF16) {
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    hipLaunchKernelGGL(gemm_bf16_kernel<KIND>, dim3((unsigned)tiles), dim3(256), 0, s,
+    hipLaunchKernelGGL(gemm_bf16_kernel<KIND>, dim3((unsigned)tiles), dim3(64 * kWaves), 0, s,
                        (const bf16*)a, (const bf16*)wt, M, N, K, e);
   } else {
     dim3 grid((unsigned)((M + 63) / 64), (unsigned)(N / 64));
