@@ -2,6 +2,7 @@
 """Benchmark: seconds per ACID-gated denoise loop at the Wan-2.1-1.3B shape.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py --workload small-dit-bf16 --sweep      (gate sweep: PSNR vs no-cache)
 
 One bench "step" is one whole denoise loop (timestep-modulation table, per
 step TEMNI + drift + gate, computed steps through all DiT blocks with the
@@ -14,9 +15,14 @@ Workload: 30 blocks, hidden 1536, 12 heads x 128, FFN 8960, 21 x 30 x 52 =
 (tau_low 0.05, tau_high 0.2, delta 0.01), random-init weights N(0, 0.02^2)
 and N(0, 1) latents (synthetic stand-ins for the trained model and prompts).
 
+Other workloads (--workload): tiny-dit-f32, small-dit-bf16,
+cogvideox-5b-shape, hunyuanvideo-slice (acid_inputs.CONFIGS).
+
 Per-kernel durations come from the library's HIP-event timer on the stream
 the kernels run on, over the timed loops.  The CPU baseline is the oracle
-(fp64 NumPy) timed on a bounded sample on this host and extrapolated.
+(fp64 NumPy) timed on this host: the whole loop for workloads of at most
+2048 tokens, else a bounded sample (one block at full K/V for a few query
+rows) extrapolated.
 """
 from __future__ import annotations
 
@@ -33,6 +39,7 @@ sys.path.insert(0, ROOT)
 METRIC = "s per denoise loop; attention/GEMM TFLOP/s (% MFMA peak) at Wan-1.3B shape"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 vector
 
 
 def log(msg: str) -> None:
@@ -73,6 +80,29 @@ def measured_traffic(kernel_source: str, record: str):
     if rec.get("source_sha256") != sha:
         return None
     return rec["hbm_bytes_per_dispatch"]
+
+
+def cpu_baseline_full(ai, cfg, schedule, gate: dict, threads: int, x_gpu) -> dict:
+    """The oracle's whole denoise loop (small workloads), forced to the GPU
+    run's schedule; also reports the relative error of the GPU's x_N."""
+    import numpy as np
+
+    import oracle as O
+
+    om = O.DiTModel(cfg, ai.weights(cfg))
+    x0 = ai.latents(cfg)
+    t0 = time.perf_counter()
+    xr, _ = O.denoise_loop(om, x0, ai.sigmas(cfg.n_steps), ai.text_tokens(cfg), mode="acid",
+                           gate=O.GateParams(gate["tau_low"], gate["tau_high"], gate["delta"]),
+                           forced_schedule=schedule)
+    t = time.perf_counter() - t0
+    d = np.asarray(x_gpu, np.float64) - x0
+    rel = float(np.linalg.norm(d - (xr - x0)) / np.linalg.norm(xr - x0))
+    log(f"cpu baseline: full oracle loop {t:.2f} s, GPU x_N - x_0 rel err {rel:.2e}")
+    return {"value": t, "unit": "s/loop", "cores": threads, "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle: the whole denoise loop ({cfg.n_steps} steps, "
+                       f"{int(np.sum(schedule))} computed, schedule forced to the GPU run's)"),
+            "gpu_rel_err_x": rel}
 
 
 def cpu_baseline(ai, cfg, n_computed: int, n_steps: int, threads: int) -> dict:
@@ -117,6 +147,68 @@ def cpu_baseline(ai, cfg, n_computed: int, n_steps: int, threads: int) -> dict:
                        f"steps of per-step work (extrapolated)")}
 
 
+def psnr(x, ref) -> float:
+    """PSNR of x against ref with peak = max(ref) - min(ref), on final latents
+    (device tensors; the quality measure of the gate sweep)."""
+    x64, r64 = x.double(), ref.double()
+    mse = float(((x64 - r64) ** 2).mean())
+    rng = float(r64.max() - r64.min())
+    return math.inf if mse == 0.0 else 10.0 * math.log10(rng * rng / mse)
+
+
+def parse_list(text: str):
+    return [float(v) for v in text.split(",") if v]
+
+
+def run_sweep(args, m, cfg, x0, text_d, sig) -> int:
+    """No-cache, fixed-threshold and ACID runs on one workload: computed
+    steps, PSNR of x_N against the no-cache x_N, seconds per loop."""
+    import statistics
+
+    import torch
+
+    x = torch.empty_like(x0)
+
+    def timed(mode, **gate):
+        times, tr = [], None
+        for k in range(args.warmup + args.steps):
+            x.copy_(x0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            tr = m.denoise_loop(x, sig, text_d, mode=mode, **gate)
+            torch.cuda.synchronize()
+            if k >= args.warmup:
+                times.append(time.perf_counter() - t0)
+        return statistics.median(times), tr
+
+    t_ref, _ = timed("nocache")
+    ref = x.clone()
+    runs = [{"mode": "nocache", "computed_steps": cfg.n_steps, "s_per_loop": t_ref,
+             "psnr_db": math.inf}]
+    grid = [("fixed", t, t, args.sweep_deltas_fixed) for t in parse_list(args.sweep_taus)]
+    for pair in args.sweep_pairs.split(","):
+        lo, hi = (float(v) for v in pair.split(":"))
+        grid += [("acid", lo, hi, d) for d in parse_list(args.sweep_deltas)]
+    for kind, lo, hi, delta in grid:
+        t, tr = timed("acid", tau_low=lo, tau_high=hi, delta=delta)
+        n_comp = int(tr["compute"].sum())
+        ds = [abs(a - b) for a, b in zip(tr["s"][2:], tr["s"][1:-1])]
+        run = {"mode": kind, "tau_low": lo, "tau_high": hi, "delta": delta,
+               "computed_steps": n_comp, "s_per_loop": t, "speedup_vs_nocache": t_ref / t,
+               "psnr_db": psnr(x, ref),
+               "steps_tau_high": int(sum(1 for v in tr["tau_used"][1:] if v == hi)),
+               "drift_s_min_max": [float(min(tr["s"][1:])), float(max(tr["s"][1:]))],
+               "drift_step_change_median_max": ([float(sorted(ds)[len(ds) // 2]), float(max(ds))]
+                                                if ds else None),
+               "schedule": "".join("C" if c else "S" for c in tr["compute"])}
+        runs.append(run)
+        log(f"{kind} tau=({lo}, {hi}) delta={delta}: {n_comp}/{cfg.n_steps} computed, "
+            f"{t * 1e3:.2f} ms/loop, PSNR {run['psnr_db']:.2f} dB")
+    print(json.dumps({"sweep": {"workload": cfg.name, "denoise_steps": cfg.n_steps,
+                                "loops_timed": args.steps, "runs": runs}}), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -130,6 +222,14 @@ def main() -> int:
     ap.add_argument("--no-nocache", action="store_true", help="skip the uncached context loop")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="disable the per-kernel event timer")
+    ap.add_argument("--sweep", action="store_true",
+                    help="gate sweep on --workload: no-cache, fixed tau, ACID tau pairs x delta "
+                         "(computed steps, PSNR vs no-cache, s/loop)")
+    ap.add_argument("--sweep-taus", default="0.05,0.1,0.2", help="fixed thresholds")
+    ap.add_argument("--sweep-pairs", default="0.05:0.2", help="ACID tau_low:tau_high pairs")
+    ap.add_argument("--sweep-deltas", default="0.0002,0.0005,0.001,0.002,0.005,0.01,0.02")
+    ap.add_argument("--sweep-deltas-fixed", type=float, default=0.01,
+                    help="delta for fixed-tau runs (unused when tau_low == tau_high)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the residual-cache store over three 1 GiB fp32 arrays (reads "
                          "2 GiB, writes 1 GiB): the reference for scaling HBM byte counters")
@@ -168,7 +268,16 @@ def main() -> int:
 
     t0 = time.perf_counter()
     m = P.Model(cfg, max_steps=N)
-    m.load_weights(ai.iter_weights(cfg))
+
+    def progress(it):
+        last = time.perf_counter()
+        for i, item in enumerate(it):
+            if time.perf_counter() - last > 20:
+                last = time.perf_counter()
+                log(f"weights: tensor {i} of {m.tensor_count()}")
+            yield item
+
+    m.load_weights(progress(ai.iter_weights(cfg)))
     torch.cuda.synchronize()
     log(f"weights generated and loaded in {time.perf_counter() - t0:.1f} s "
         f"(arena {m.arena.numel() / 2**30:.2f} GiB, workspace {m.workspace.numel() / 2**30:.2f} GiB)")
@@ -178,6 +287,9 @@ def main() -> int:
     sig = ai.sigmas(N)
     x = torch.empty_like(x0)
     gate = dict(tau_low=args.tau_low, tau_high=args.tau_high, delta=args.delta)
+
+    if args.sweep:
+        return run_sweep(args, m, cfg, x0, text_d, sig)
 
     for w in range(args.warmup):
         x.copy_(x0)
@@ -217,7 +329,10 @@ def main() -> int:
             rate = amount * args.steps / (ms * 1e-3)
             if kind == "flop":
                 ent["tflops"] = rate / 1e12
-                ent["frac_bf16_peak"] = rate / 1e12 / PEAK_BF16_TFLOPS
+                if cfg.dtype == "bf16":
+                    ent["frac_bf16_peak"] = rate / 1e12 / PEAK_BF16_TFLOPS
+                else:
+                    ent["frac_f32_peak"] = rate / 1e12 / PEAK_F32_TFLOPS
             else:
                 ent["gbs"] = rate / 1e9
                 ent["frac_hbm_peak"] = rate / 1e9 / PEAK_HBM_GBS
@@ -236,10 +351,13 @@ def main() -> int:
         if cfg.head_dim == 128 and cfg.name == "wan2.1-1.3b-shape":
             traffic = measured_traffic("paper_2607_12358_amd/csrc/attention.hip",
                                        "profiles/attention_counters.json")
-        roofline = {"bound": "mfma", "achieved": ach, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": ach / PEAK_BF16_TFLOPS, "traffic": traffic,
-                    "kernel": "attn_bf16_kernel<128>", "flop_per_launch": per_launch,
-                    "avg_launch_us": avg_s * 1e6}
+        if cfg.dtype == "bf16":
+            bound, peak, kname = "mfma", PEAK_BF16_TFLOPS, f"attn_bf16_kernel<{cfg.head_dim}>"
+        else:  # fp32 attention runs on the vector ALUs
+            bound, peak, kname = "alu", PEAK_F32_TFLOPS, f"attn_f32_kernel<{cfg.head_dim}>"
+        roofline = {"bound": bound, "achieved": ach, "peak": peak, "unit": "TFLOP/s",
+                    "frac": ach / peak, "traffic": traffic, "kernel": kname,
+                    "flop_per_launch": per_launch, "avg_launch_us": avg_s * 1e6}
 
     nocache = None
     if not args.no_nocache:
@@ -259,7 +377,13 @@ def main() -> int:
                            if i.get("user_api") == "blas"), default=1)
         except Exception:
             threads = len(os.sched_getaffinity(0))
-        cpu = cpu_baseline(ai, cfg, n_comp, N, threads)
+        if cfg.n_tokens <= 2048:
+            x.copy_(x0)
+            m.denoise_loop(x, sig, text_d, mode="acid", **gate)
+            cpu = cpu_baseline_full(ai, cfg, traces[-1]["compute"], gate, threads,
+                                    x.cpu().numpy())
+        else:
+            cpu = cpu_baseline(ai, cfg, n_comp, N, threads)
 
     out = {
         "metric": METRIC,
@@ -282,7 +406,8 @@ def main() -> int:
         "computed_steps": n_comp,
         "schedule": "".join("C" if c else "S" for c in traces[-1]["compute"]),
         "gemm_tflops": gemm_tflops,
-        "gemm_frac_bf16_peak": gemm_tflops / PEAK_BF16_TFLOPS if gemm_tflops else None,
+        "gemm_frac_peak": (gemm_tflops / (PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else
+                                          PEAK_F32_TFLOPS)) if gemm_tflops else None,
         "kernels": kernels,
         "nocache_s_per_loop": nocache,
         "speedup_vs_nocache": (nocache / s_per_loop) if nocache else None,
