@@ -22,6 +22,9 @@ What is computed, and where it comes from
 * Skipped steps reuse the previous output corrected by a stored residual
   (same paragraph): on a computed step r = h_out - x, on a skipped step
   h_out = x + r.
+* EasyCache's signal under the same gate (``easycache_loop``): Section 2,
+  paragraph "EasyCache" (transformation rate k, signal k |dx| / |v_prev|,
+  reuse v = x + D) and Section 3.3 (the gated variable); L1 norms.
 * The backbone f_theta (Algorithm 1 treats it as a black box) is an adaLN
   DiT: sinusoidal timestep embedding -> MLP -> per-block shift/scale/gate
   modulation, LayerNorm without affine parameters, full non-causal multi-head
@@ -328,6 +331,66 @@ def gate_schedule(s_seq: Sequence[float], p: GateParams):
 TRACE_DTYPE = np.dtype([("compute", np.int32), ("gate_compute", np.int32),
                         ("s", np.float64), ("sigma_sum_after", np.float64),
                         ("tau_used", np.float64)])
+
+
+def l1_norm(a: np.ndarray) -> float:
+    """sum |a| in float64."""
+    return float(np.abs(np.asarray(a, F64)).sum())
+
+
+def ratio_or_inf(num: float, den: float) -> float:
+    """num / den with 0/0 = 0 and num/0 = +inf (num >= 0)."""
+    if den == 0.0:
+        return 0.0 if num == 0.0 else math.inf
+    return num / den
+
+
+def easycache_loop(forward: Callable, x0: np.ndarray, sigmas: np.ndarray,
+                   gate: Optional[GateParams] = None, mode: str = "easycache",
+                   forced_schedule: Optional[Sequence[int]] = None):
+    """EasyCache's signal under the gate of Algorithm 1 (Section 2, paragraph
+    "EasyCache"; Section 3.3 for the gated variable).
+
+    forward(x, sigma) -> v runs the whole model.  On a computed step i >= 1
+    the transformation rate is k = |v_i - v_{i-1}|_1 / |x_i - x_{i-1}|_1 (output
+    change over input change at that step) and the offset D = v_i - x_i is
+    stored.  At step i the signal is s_i = k |x_i - x_{i-1}|_1 / |v_{i-1}|_1
+    with k from the last computed step; a skipped step outputs v_i = x_i + D.
+    The first n_warmup >= 2 steps run the model (k needs two).  Norms are L1.
+    mode "nocache" runs the model on every step.  Returns (x_N, trace).
+    """
+    n = len(sigmas) - 1
+    if mode == "easycache" and (gate is None or gate.n_warmup < 2):
+        raise ValueError("EasyCache needs n_warmup >= 2")
+    g = AcidGate(gate) if mode == "easycache" else None
+    x = np.asarray(x0, dtype=F64)
+    x_prev = v_prev = offset = None
+    k = None
+    trace = np.zeros(n, dtype=TRACE_DTYPE)
+    for i in range(n):
+        sig = float(sigmas[i])
+        s = math.nan
+        if mode == "nocache":
+            gate_compute, tau = True, math.nan
+        else:
+            if k is not None:
+                s = k * ratio_or_inf(l1_norm(x - x_prev), l1_norm(v_prev))
+            gate_compute, tau = g(s)
+        compute = gate_compute if forced_schedule is None else bool(forced_schedule[i])
+        if compute:
+            v = np.asarray(forward(x, sig), dtype=F64)
+            if v_prev is not None:
+                k = ratio_or_inf(l1_norm(v - v_prev), l1_norm(x - x_prev))
+            offset = v - x
+        else:
+            if offset is None:
+                raise ValueError("skip requested before any computed step")
+            v = x + offset
+        x_prev, v_prev = x, v
+        x = x + (float(sigmas[i + 1]) - sig) * v
+        trace[i] = (int(compute), int(gate_compute), s,
+                    g.sigma_sum if g is not None else 0.0, tau)
+    return x, trace
 
 
 def denoise_loop(model, x0: np.ndarray, sigmas: np.ndarray, text=None,
