@@ -53,8 +53,19 @@ typedef enum {
 typedef enum { ACID_F32 = 0, ACID_BF16 = 1 } acid_dtype;
 
 /* NOCACHE runs f_theta on every step and forms no signal.  ACID runs
- * Algorithm 1; a fixed threshold is ACID with tau_low == tau_high. */
-typedef enum { ACID_MODE_NOCACHE = 0, ACID_MODE_ACID = 1 } acid_mode;
+ * Algorithm 1 on TeaCache's signal; a fixed threshold is ACID with
+ * tau_low == tau_high.  EASYCACHE runs Algorithm 1 on EasyCache's signal
+ * (Section 2, paragraph "EasyCache"; Section 3.3 names it as the gated
+ * variable): transformation rate k = |v_i - v_{i-1}|_1 / |x_i - x_{i-1}|_1 on
+ * each computed step i >= 1, signal s_i = k |x_i - x_{i-1}|_1 / |v_{i-1}|_1
+ * with k of the last computed step, and a skipped step outputs
+ * v_i = x_i + D with D = v - x of the last computed step (the whole model,
+ * head included, is skipped).  Needs gate->n_warmup >= 2. */
+typedef enum {
+  ACID_MODE_NOCACHE = 0,
+  ACID_MODE_ACID = 1,
+  ACID_MODE_EASYCACHE = 2
+} acid_mode;
 
 /* Residual cache (TeaCache's reuse rule).  STORE on a computed step:
  * r = h_out - x.  APPLY on a skipped step: h_out = x + r. */
@@ -222,6 +233,22 @@ acid_status acid_cache_apply(acid_cache_op op, const float* x_dev,
                              float* h_out_dev, float* r_dev, int64_t n,
                              hipStream_t stream);
 
+/* L1 sums for EasyCache's signal, in one pass over n fp32 elements:
+ * out_host[0] = sum |a - b| (sum |a| if b_dev is NULL), out_host[1] =
+ * sum |c| (0 if c_dev is NULL).  fp64 accumulation in a fixed order
+ * (deterministic).  Uses the model's workspace for partial sums, so n must
+ * be at most n_video * hidden.  Synchronises the stream. */
+acid_status acid_l1_norms(acid_model* m, const float* a_dev, const float* b_dev,
+                          const float* c_dev, int64_t n, double* out_host,
+                          hipStream_t stream);
+
+/* EasyCache's skipped step over n fp32 elements: v = x + D; x_prev = x;
+ * x = x + dsigma v (x updated in place; v_dev and x_prev_dev written;
+ * offset_dev D read).  The four buffers must not overlap. */
+acid_status acid_easycache_reuse(float* x_dev, float* x_prev_dev, float* v_dev,
+                                 const float* offset_dev, int64_t n, float dsigma,
+                                 hipStream_t stream);
+
 /* The denoise loop of Algorithm 1 around f_theta, n_steps steps over noise
  * levels sigmas_host[0..n_steps] (host fp32).  x_dev fp32 [L_v][H]: x_0 in,
  * x_N out.  Per step i: (ACID mode) TEMNI + drift s_i, gate; compute -> all
@@ -230,7 +257,12 @@ acid_status acid_cache_apply(acid_cache_op op, const float* x_dev,
  * gate may be NULL in NOCACHE mode.  forced_schedule_host (NULL or n_steps
  * bytes, 0/1) overrides the executed decision while the gate keeps its own
  * state; its step 0 must be 1.  trace_host (NULL or n_steps entries)
- * receives the per-step trace.  One stream synchronisation per ACID step. */
+ * receives the per-step trace.  One stream synchronisation per ACID step.
+ * EASYCACHE mode: per step i >= 1 the L1 sums |x_i - x_{i-1}|, |v_{i-1}| give
+ * s_i (NaN until a rate k exists), then the gate; compute -> f_theta, x
+ * update by the head's Euler epilogue, D = v_i - x_i and (i >= 1) the new
+ * k; skip -> acid_easycache_reuse.  The TEMNI buffers of the workspace hold
+ * x_{i-1} and v_{i-1}.  Two stream synchronisations per computed step. */
 acid_status acid_denoise_loop(acid_model* m, float* x_dev,
                               const float* sigmas_host, int32_t n_steps,
                               const float* text_dev, int32_t mode,

@@ -15,11 +15,12 @@ import numpy as np
 from . import _lib as _L
 from ._lib import (ACID_BF16, ACID_CACHE_APPLY, ACID_CACHE_STORE, ACID_EPI_BIAS,  # noqa: F401
                    ACID_EPI_BIAS_GELU, ACID_EPI_EULER, ACID_EPI_GATE_RESIDUAL, ACID_EPI_QKV,
-                   ACID_F32, ACID_MODE_ACID, ACID_MODE_NOCACHE, KERNEL_CLASSES, AcidError,
+                   ACID_F32, ACID_MODE_ACID, ACID_MODE_EASYCACHE, ACID_MODE_NOCACHE,
+                   KERNEL_CLASSES, AcidError,
                    TRACE_DTYPE, check, lib)
 
-__all__ = ["Model", "gate", "GateState", "cache_apply", "attention", "linear", "ln_modulate",
-           "version", "AcidError", "KERNEL_CLASSES"]
+__all__ = ["Model", "gate", "GateState", "cache_apply", "easycache_reuse", "attention", "linear",
+           "ln_modulate", "version", "AcidError", "KERNEL_CLASSES"]
 
 
 def _torch():
@@ -80,6 +81,15 @@ def cache_apply(op: int, x, h_out, r, stream=None) -> None:
     if h_out.numel() != n or r.numel() != n:
         raise ValueError("x, h_out and r must have the same number of elements")
     check(lib().acid_cache_apply(op, _ptr(x), _ptr(h_out), _ptr(r), n, _stream(stream)))
+
+
+def easycache_reuse(x, x_prev, v, offset, dsigma: float, stream=None) -> None:
+    """EasyCache's skipped step: v = x + offset; x_prev = x; x += dsigma v."""
+    n = x.numel()
+    if x_prev.numel() != n or v.numel() != n or offset.numel() != n:
+        raise ValueError("x, x_prev, v and offset must have the same number of elements")
+    check(lib().acid_easycache_reuse(_ptr(x), _ptr(x_prev), _ptr(v), _ptr(offset), n,
+                                     float(dsigma), _stream(stream)))
 
 
 def ln_modulate(x, shift, scale, out, stream=None) -> None:
@@ -184,13 +194,29 @@ class Model:
                                       C.byref(s), _stream(stream)))
         return s.value
 
+    def l1_norms(self, a, b=None, c=None, stream=None):
+        """(sum |a - b| or sum |a|, sum |c| or 0) in fp64, deterministic."""
+        out = (C.c_double * 2)()
+        check(lib().acid_l1_norms(self.h, _ptr(a), _ptr(b), _ptr(c), a.numel(), out,
+                                  _stream(stream)))
+        return out[0], out[1]
+
     def denoise_loop(self, x, sigmas: Sequence[float], text=None, mode: str = "acid",
                      tau_low: float = 0.05, tau_high: float = 0.2, delta: float = 0.01,
-                     n_warmup: int = 1, forced_schedule=None, stream=None) -> np.ndarray:
-        """Runs the loop in place on x; returns the per-step trace."""
+                     n_warmup: Optional[int] = None, forced_schedule=None,
+                     stream=None) -> np.ndarray:
+        """Runs the loop in place on x; returns the per-step trace.  mode is
+        "nocache", "acid" (TeaCache's signal) or "easycache"; n_warmup
+        defaults to 1 (2 for "easycache")."""
         sig = np.ascontiguousarray(sigmas, dtype=np.float32)
         n = len(sig) - 1
-        modec = ACID_MODE_ACID if mode == "acid" else ACID_MODE_NOCACHE
+        modes = {"acid": ACID_MODE_ACID, "nocache": ACID_MODE_NOCACHE,
+                 "easycache": ACID_MODE_EASYCACHE}
+        if mode not in modes:
+            raise ValueError(f"unknown mode {mode!r}")
+        modec = modes[mode]
+        if n_warmup is None:
+            n_warmup = 2 if mode == "easycache" else 1
         p = _L.GateParamsC(tau_low, tau_high, delta, n_warmup)
         tr = (_L.StepTraceC * n)()
         forced = None

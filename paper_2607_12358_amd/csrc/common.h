@@ -81,6 +81,10 @@ hipError_t launch_drift_finalize(const double* partials, int64_t rows, double* o
 hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n,
                         hipStream_t s);
 // fp32 [in][out] -> [out][in] in dtype
+hipError_t launch_l1_norms(const float* a, const float* b, const float* c, int64_t n,
+                           double* partials, int max_groups, double* out, hipStream_t s);
+hipError_t launch_easycache_reuse(float* x, float* xp, float* v, const float* d, int64_t n,
+                                  float dsig, hipStream_t s);
 hipError_t launch_transpose_convert(const float* src, int64_t in, int64_t out, int dtype,
                                     void* dst, hipStream_t s);
 

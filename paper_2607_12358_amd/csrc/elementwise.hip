@@ -196,6 +196,115 @@ __global__ __launch_bounds__(256) void cache_kernel(const float* __restrict__ x,
   }
 }
 
+// L1 partial sums in fp64 for EasyCache's signal: block g accumulates
+// sum |a - b| (sum |a| without b) and sum |c| over its grid-stride share;
+// part[2g], part[2g+1].  The grid depends on n only, and every sum has a
+// fixed order, so the result is deterministic.
+__device__ __forceinline__ double block_sum_f64(double v, double* lds) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) lds[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  if (threadIdx.x == 0)
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += lds[i];
+  return t;
+}
+
+template <bool HAS_B, bool HAS_C>
+__global__ __launch_bounds__(256) void l1_partials_kernel(const float* __restrict__ a,
+                                                          const float* __restrict__ b,
+                                                          const float* __restrict__ c,
+                                                          int64_t n, double* __restrict__ part) {
+  __shared__ double lds[4];
+  const int64_t n4 = n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const float4* a4 = reinterpret_cast<const float4*>(a);
+  const float4* b4 = reinterpret_cast<const float4*>(b);
+  const float4* c4 = reinterpret_cast<const float4*>(c);
+  double s0 = 0.0, s1 = 0.0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    float4 av = a4[i];
+    if (HAS_B) {
+      const float4 bv = b4[i];
+      av = make_float4(av.x - bv.x, av.y - bv.y, av.z - bv.z, av.w - bv.w);
+    }
+    s0 += ((double)fabsf(av.x) + (double)fabsf(av.y)) + ((double)fabsf(av.z) + (double)fabsf(av.w));
+    if (HAS_C) {
+      const float4 cv = c4[i];
+      s1 += ((double)fabsf(cv.x) + (double)fabsf(cv.y)) + ((double)fabsf(cv.z) + (double)fabsf(cv.w));
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
+    const int64_t i = n4 * 4 + threadIdx.x;
+    s0 += (double)fabsf(HAS_B ? a[i] - b[i] : a[i]);
+    if (HAS_C) s1 += (double)fabsf(c[i]);
+  }
+  s0 = block_sum_f64(s0, lds);
+  s1 = block_sum_f64(s1, lds);
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = s0;
+    part[2 * blockIdx.x + 1] = s1;
+  }
+}
+
+// Fixed-order sum of G partial pairs: out[0], out[1].
+__global__ __launch_bounds__(1024) void l1_finalize_kernel(const double* __restrict__ part, int G,
+                                                           double* __restrict__ out) {
+  __shared__ double s0[1024], s1[1024];
+  const int t = threadIdx.x;
+  double u = 0.0, w = 0.0;
+  for (int g = t; g < G; g += 1024) {
+    u += part[2 * g];
+    w += part[2 * g + 1];
+  }
+  s0[t] = u;
+  s1[t] = w;
+  __syncthreads();
+  for (int k = 512; k > 0; k >>= 1) {
+    if (t < k) {
+      s0[t] += s0[t + k];
+      s1[t] += s1[t + k];
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    out[0] = s0[0];
+    out[1] = s1[0];
+  }
+}
+
+// EasyCache's skipped step: v = x + D; x_prev = x; x = x + dsigma v.
+__global__ __launch_bounds__(256) void easycache_reuse_kernel(float* __restrict__ x,
+                                                              float* __restrict__ xp,
+                                                              float* __restrict__ v,
+                                                              const float* __restrict__ d,
+                                                              int64_t n, float dsig) {
+  const int64_t n4 = n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  float4* x4 = reinterpret_cast<float4*>(x);
+  float4* p4 = reinterpret_cast<float4*>(xp);
+  float4* v4 = reinterpret_cast<float4*>(v);
+  const float4* d4 = reinterpret_cast<const float4*>(d);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    const float4 a = x4[i], o = d4[i];
+    const float4 w = make_float4(a.x + o.x, a.y + o.y, a.z + o.z, a.w + o.w);
+    p4[i] = a;
+    v4[i] = w;
+    x4[i] = make_float4(fmaf(dsig, w.x, a.x), fmaf(dsig, w.y, a.y), fmaf(dsig, w.z, a.z),
+                        fmaf(dsig, w.w, a.w));
+  }
+  if (blockIdx.x == 0 && threadIdx.x < (n & 3)) {
+    const int64_t i = n4 * 4 + threadIdx.x;
+    const float a = x[i], w = a + d[i];
+    xp[i] = a;
+    v[i] = w;
+    x[i] = fmaf(dsig, w, a);
+  }
+}
+
 // fp32 [in][out] -> [out][in] (dtype), 32x32 tiles through LDS.
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_convert_kernel(const float* __restrict__ src,
@@ -286,6 +395,38 @@ hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n, h
     hipLaunchKernelGGL(cache_kernel<ACID_CACHE_STORE>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
   else
     hipLaunchKernelGGL(cache_kernel<ACID_CACHE_APPLY>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
+  return hipGetLastError();
+}
+
+static int l1_grid(int64_t n, int max_groups) {
+  int64_t g = ((n >> 2) + 255) / 256;
+  if (g < 1) g = 1;
+  if (g > 1024) g = 1024;
+  if (g > max_groups) g = max_groups;
+  return (int)g;
+}
+
+hipError_t launch_l1_norms(const float* a, const float* b, const float* c, int64_t n,
+                           double* partials, int max_groups, double* out, hipStream_t s) {
+  const int G = l1_grid(n, max_groups);
+#define L1K(HB, HC) \
+  hipLaunchKernelGGL((l1_partials_kernel<HB, HC>), dim3(G), dim3(256), 0, s, a, b, c, n, partials)
+  if (b && c) L1K(true, true);
+  else if (b) L1K(true, false);
+  else if (c) L1K(false, true);
+  else L1K(false, false);
+#undef L1K
+  hipLaunchKernelGGL(l1_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, G, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_easycache_reuse(float* x, float* xp, float* v, const float* d, int64_t n,
+                                  float dsig, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  int64_t blocks = ((n + 3) / 4 + 255) / 256;
+  if (blocks > 256 * 16) blocks = 256 * 16;
+  hipLaunchKernelGGL(easycache_reuse_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, xp, v, d,
+                     n, dsig);
   return hipGetLastError();
 }
 

@@ -373,6 +373,91 @@ acid_status drift(acid_model* m, const float* row, const float* x, const float* 
   });
 }
 
+// sum |a - b| (or |a|) and sum |c| (or 0) over n elements into out2 (host).
+acid_status l1_norms(acid_model* m, const float* a, const float* b, const float* c, int64_t n,
+                     double* out2, hipStream_t s) {
+  double* part = m->kp<double>(m->kl.partials);
+  double* dres = m->kp<double>(m->kl.dres);
+  const int max_groups = (int)(m->Lv() < 1024 ? m->Lv() : 1024);
+  ACID_TRY(run(m, ACID_K_DRIFT, s, "l1 norms", [&]() {
+    return launch_l1_norms(a, b, c, n, part, max_groups, dres, s);
+  }));
+  ACID_HIP(hipMemcpyAsync(out2, dres, 2 * sizeof(double), hipMemcpyDeviceToHost, s));
+  ACID_HIP(hipStreamSynchronize(s));
+  return ACID_OK;
+}
+
+double ratio_or_inf(double num, double den) {
+  if (den == 0.0) return num == 0.0 ? 0.0 : INFINITY;
+  return num / den;
+}
+
+// EasyCache's signal under Algorithm 1 (see acid_mode): the workspace's
+// TEMNI buffers hold x_{i-1} (m0) and the previous output (ping-pong with v),
+// the residual buffer holds the offset D.
+acid_status easycache_loop(acid_model* m, float* x, const float* sig, int n, const float* text,
+                           const acid_gate_params* gate, const uint8_t* forced,
+                           acid_step_trace* trace, hipStream_t s) {
+  const int H = m->H();
+  const int64_t nv = m->Lv() * H;
+  float* table = m->kp(m->kl.modtab);
+  float* xprev = m->kp(m->kl.m0);
+  float* vbuf[2] = {m->kp(m->kl.v), m->kp(m->kl.m1)};
+  float* offset = m->kp(m->kl.r);
+  float* hv = m->kp(m->kl.h) + m->Lt() * H;
+  ACID_TRY(modulation_table(m, sig, n, table, s));
+  acid_gate_state st = {};
+  double k = NAN;
+  bool have_k = false, have_offset = false;
+  int cur = 0;  // vbuf[cur] receives v_i, vbuf[cur ^ 1] holds v_{i-1}
+  for (int i = 0; i < n; ++i) {
+    const float* row = table + (int64_t)i * m->rowsz();
+    double si = NAN, tau = NAN, dx = NAN;
+    if (i > 0) {
+      double sums[2];
+      ACID_TRY(l1_norms(m, x, xprev, vbuf[cur ^ 1], nv, sums, s));
+      dx = sums[0];
+      if (have_k) si = k * ratio_or_inf(sums[0], sums[1]);
+    }
+    int32_t gate_compute = 1;
+    ACID_TRY(acid_gate(&st, gate, si, &gate_compute, &tau));
+    const int compute = forced ? (forced[i] != 0) : gate_compute;
+    const float dsig = sig[i + 1] - sig[i];
+    float* v = vbuf[cur];
+    if (compute) {
+      ACID_TRY(run(m, ACID_K_MISC, s, "keep x_i", [&]() {
+        return hipMemcpyAsync(xprev, x, nv * sizeof(float), hipMemcpyDeviceToDevice, s);
+      }));
+      ACID_TRY(stack_forward(m, row, x, text, s));
+      ACID_TRY(head_forward(m, row, hv, v, x, dsig, s));  // v_i; x <- x_{i+1}
+      ACID_TRY(run(m, ACID_K_CACHE, s, "offset store", [&]() {
+        return launch_cache(ACID_CACHE_STORE, xprev, v, offset, nv, s);  // D = v_i - x_i
+      }));
+      have_offset = true;
+      if (i > 0) {
+        double sums[2];
+        ACID_TRY(l1_norms(m, v, vbuf[cur ^ 1], nullptr, nv, sums, s));
+        k = ratio_or_inf(sums[0], dx);
+        have_k = true;
+      }
+    } else {
+      if (!have_offset) return set_error(ACID_ERR_INVALID_ARG, "skip before any computed step");
+      ACID_TRY(run(m, ACID_K_CACHE, s, "easycache reuse", [&]() {
+        return launch_easycache_reuse(x, xprev, v, offset, nv, dsig, s);
+      }));
+    }
+    cur ^= 1;
+    if (trace) {
+      trace[i].compute = compute;
+      trace[i].gate_compute = gate_compute;
+      trace[i].s = si;
+      trace[i].sigma_sum_after = st.sigma_sum;
+      trace[i].tau_used = tau;
+    }
+  }
+  return ACID_OK;
+}
+
 acid_status read_drift(acid_model* m, double* s_out, hipStream_t s) {
   double res[3];
   ACID_HIP(hipMemcpyAsync(res, m->kp<double>(m->kl.dres), sizeof res, hipMemcpyDeviceToHost, s));
@@ -621,6 +706,33 @@ acid_status acid_block_forward(acid_model* m, int32_t block, const float* mod6_d
   return block_forward(m, block, mod6_dev, h_dev, stream);
 }
 
+acid_status acid_l1_norms(acid_model* m, const float* a_dev, const float* b_dev,
+                          const float* c_dev, int64_t n, double* out_host, hipStream_t stream) {
+  if (!m || !a_dev || !out_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (n < 0 || n > m->Lv() * m->H())
+    return set_error(ACID_ERR_INVALID_ARG, "n %lld outside [0, n_video * hidden]", (long long)n);
+  if (((uintptr_t)a_dev | (uintptr_t)b_dev | (uintptr_t)c_dev) % 16)
+    return set_error(ACID_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
+  if (n == 0) {
+    out_host[0] = out_host[1] = 0.0;
+    return ACID_OK;
+  }
+  return l1_norms(m, a_dev, b_dev, c_dev, n, out_host, stream);
+}
+
+acid_status acid_easycache_reuse(float* x_dev, float* x_prev_dev, float* v_dev,
+                                 const float* offset_dev, int64_t n, float dsigma,
+                                 hipStream_t stream) {
+  if (n < 0) return set_error(ACID_ERR_INVALID_ARG, "n < 0");
+  if (n == 0) return ACID_OK;
+  if (!x_dev || !x_prev_dev || !v_dev || !offset_dev)
+    return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (((uintptr_t)x_dev | (uintptr_t)x_prev_dev | (uintptr_t)v_dev | (uintptr_t)offset_dev) % 16)
+    return set_error(ACID_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
+  hipError_t e = launch_easycache_reuse(x_dev, x_prev_dev, v_dev, offset_dev, n, dsigma, stream);
+  return e == hipSuccess ? ACID_OK : check_hip(e, "easycache reuse");
+}
+
 acid_status acid_cache_apply(acid_cache_op op, const float* x_dev, float* h_out_dev, float* r_dev,
                              int64_t n, hipStream_t stream) {
   if (op != ACID_CACHE_STORE && op != ACID_CACHE_APPLY)
@@ -671,9 +783,13 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev, const float* sigmas_h
                               const acid_gate_params* gate, const uint8_t* forced,
                               acid_step_trace* trace, hipStream_t stream) {
   if (!m || !x_dev || !sigmas_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
-  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID)
+  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID && mode != ACID_MODE_EASYCACHE)
     return set_error(ACID_ERR_INVALID_ARG, "bad mode %d", mode);
-  if (mode == ACID_MODE_ACID && !gate) return set_error(ACID_ERR_INVALID_ARG, "gate params NULL");
+  if (mode != ACID_MODE_NOCACHE && !gate)
+    return set_error(ACID_ERR_INVALID_ARG, "gate params NULL");
+  if (mode == ACID_MODE_EASYCACHE && gate->n_warmup < 2)
+    return set_error(ACID_ERR_INVALID_ARG, "EasyCache needs n_warmup >= 2 (got %d)",
+                     gate->n_warmup);
   if (n_steps < 1 || n_steps > m->max_steps)
     return set_error(ACID_ERR_INVALID_ARG, "n_steps %d must be in [1, max_steps=%d]", n_steps,
                      m->max_steps);
@@ -683,6 +799,9 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev, const float* sigmas_h
     return set_error(ACID_ERR_INVALID_ARG, "forced schedule must compute step 0");
   if (forced && mode == ACID_MODE_NOCACHE)
     return set_error(ACID_ERR_UNSUPPORTED, "a forced schedule needs ACID mode (the residual cache)");
+
+  if (mode == ACID_MODE_EASYCACHE)
+    return easycache_loop(m, x_dev, sigmas_host, n_steps, text_dev, gate, forced, trace, stream);
 
   const int H = m->H();
   const int64_t nv = m->Lv() * H;

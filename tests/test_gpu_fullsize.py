@@ -148,6 +148,28 @@ def test_drift_fullsize_wan(P, wan_block):
     assert s == m.drift_signal(to_dev(x1), 0.98, m0, m1)  # deterministic
 
 
+def test_l1_norms_and_reuse_fullsize_wan(P, wan_block):
+    cfg, m, _ = wan_block
+    n = cfg.n_video * cfg.hidden
+    a = _seeded((n,), 41, dtype=torch.float32)
+    b = _seeded((n,), 42, dtype=torch.float32)
+    c = _seeded((n,), 43, dtype=torch.float32)
+    got = m.l1_norms(a, b, c)
+    ref0 = float((a.double() - b.double()).abs().sum())
+    ref1 = float(c.double().abs().sum())
+    assert got[0] == pytest.approx(ref0, rel=1e-6) and got[1] == pytest.approx(ref1, rel=1e-12)
+    assert m.l1_norms(a, b, c) == got
+    x0 = a.clone()
+    xp = torch.empty_like(a)
+    v = torch.empty_like(a)
+    P.easycache_reuse(a, xp, v, b, -0.02)
+    torch.cuda.synchronize()
+    idx = torch.from_numpy(np.random.default_rng(6).integers(0, n, 200000)).cuda()
+    assert torch.equal(v[idx], x0[idx] + b[idx]) and torch.equal(xp[idx], x0[idx])
+    np.testing.assert_allclose(to_np(a[idx]), to_np(x0[idx]) + -0.02 * to_np(v[idx]),
+                               rtol=1e-6, atol=1e-6)
+
+
 def test_cache_fullsize_wan(P):
     n = ai.WAN13B.n_video * ai.WAN13B.hidden
     x = _seeded((n,), 31, dtype=torch.float32)
@@ -186,6 +208,16 @@ def test_denoise_loop_wan_fullsize_properties(P):
     tr3 = m.denoise_loop(x3, sig, mode="acid", tau_low=math.inf, tau_high=math.inf, delta=0.01)
     assert int(tr3["compute"].sum()) == 1 and tr3["compute"][0] == 1
     assert math.isnan(tr["s"][0])  # no drift before the first step
+    # the EasyCache signal under the same gate, as the benchmark runs it
+    xe = x0.clone()
+    tre = m.denoise_loop(xe, sig, mode="easycache", tau_low=0.1, tau_high=0.2, delta=0.01)
+    dec, _, _ = O.gate_schedule(list(tre["s"]), O.GateParams(0.1, 0.2, 0.01, 2))
+    assert list(tre["gate_compute"].astype(bool)) == dec
+    assert np.all(np.isfinite(tre["s"][2:])) and np.all(np.isfinite(to_np(xe)))
+    xi = x0.clone()
+    tri = m.denoise_loop(xi, sig, mode="easycache", tau_low=math.inf, tau_high=math.inf,
+                         delta=0.01)
+    assert list(tri["compute"]) == [1, 1] + [0] * (cfg.n_steps - 2)
 
 
 def test_denoise_loop_small_bf16_vs_oracle(P):
