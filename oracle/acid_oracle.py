@@ -22,6 +22,10 @@ What is computed, and where it comes from
 * Skipped steps reuse the previous output corrected by a stored residual
   (same paragraph): on a computed step r = h_out - x, on a skipped step
   h_out = x + r.
+* DiCache's probe signal under the same gate (``dicache_loop``): Section 2,
+  paragraph "DiCache" (shallow probe of the first blocks every step, relative
+  change of its features, deep-output reuse on skipped steps) and Section
+  3.3; the reuse adds the stored deep residual to the probe output.
 * EasyCache's signal under the same gate (``easycache_loop``): Section 2,
   paragraph "EasyCache" (transformation rate k, signal k |dx| / |v_prev|,
   reuse v = x + D) and Section 3.3 (the gated variable); L1 norms.
@@ -390,6 +394,55 @@ def easycache_loop(forward: Callable, x0: np.ndarray, sigmas: np.ndarray,
         x = x + (float(sigmas[i + 1]) - sig) * v
         trace[i] = (int(compute), int(gate_compute), s,
                     g.sigma_sum if g is not None else 0.0, tau)
+    return x, trace
+
+
+def dicache_loop(model, x0: np.ndarray, sigmas: np.ndarray, text=None,
+                 gate: Optional[GateParams] = None, n_probe: int = 1,
+                 forced_schedule: Optional[Sequence[int]] = None):
+    """DiCache's probe signal under the gate of Algorithm 1 (Section 2,
+    paragraph "DiCache"; Section 3.3 names the probe-feature change as the
+    gated variable).
+
+    Every step runs the first n_probe blocks (the shallow probe) on
+    [text; x_i]; the signal is the relative L1 change of the probe's video
+    rows p_i against p_{i-1}.  A computed step runs the remaining blocks and
+    stores the deep residual R = h_out_v - p_i; a skipped step uses
+    h_out_v = p_i + R.  Head and Euler update on every step.  Returns
+    (x_N, trace).
+    """
+    cfg = model.cfg
+    if not 0 <= n_probe <= cfg.n_blocks:
+        raise ValueError("n_probe must be in [0, n_blocks]")
+    n = len(sigmas) - 1
+    g = AcidGate(gate)
+    x = np.asarray(x0, dtype=F64)
+    n_text = 0 if text is None else len(text)
+    p_prev = r_deep = None
+    trace = np.zeros(n, dtype=TRACE_DTYPE)
+    for i in range(n):
+        sig = float(sigmas[i])
+        mod = model.modulation(sig)
+        h = x if n_text == 0 else np.concatenate([np.asarray(text, F64), x], axis=0)
+        for b in range(n_probe):
+            h = model.block(h, b, mod["blocks"][b])
+        p = h[n_text:]
+        s = relative_l1_drift(p, p_prev) if p_prev is not None else math.nan
+        p_prev = p
+        gate_compute, tau = g(s)
+        compute = gate_compute if forced_schedule is None else bool(forced_schedule[i])
+        if compute:
+            for b in range(n_probe, cfg.n_blocks):
+                h = model.block(h, b, mod["blocks"][b])
+            h_out_v = h[n_text:]
+            r_deep = h_out_v - p
+        else:
+            if r_deep is None:
+                raise ValueError("skip requested before any computed step")
+            h_out_v = p + r_deep
+        v = model.head(h_out_v, sig)
+        x = x + (float(sigmas[i + 1]) - sig) * v
+        trace[i] = (int(compute), int(gate_compute), s, g.sigma_sum, tau)
     return x, trace
 
 
