@@ -83,7 +83,7 @@ def measured_traffic(kernel_source: str, record: str):
 
 
 def cpu_baseline_full(ai, cfg, schedule, gate: dict, threads: int, x_gpu,
-                      mode: str = "acid") -> dict:
+                      mode: str = "acid", probe_blocks: int = 1) -> dict:
     """The oracle's whole denoise loop (small workloads), forced to the GPU
     run's schedule; also reports the relative error of the GPU's x_N."""
     import numpy as np
@@ -94,7 +94,12 @@ def cpu_baseline_full(ai, cfg, schedule, gate: dict, threads: int, x_gpu,
     x0 = ai.latents(cfg)
     text = ai.text_tokens(cfg)
     t0 = time.perf_counter()
-    if mode == "easycache":
+    if mode == "dicache":
+        xr, _ = O.dicache_loop(om, x0, ai.sigmas(cfg.n_steps), text,
+                               gate=O.GateParams(gate["tau_low"], gate["tau_high"],
+                                                 gate["delta"]),
+                               n_probe=probe_blocks, forced_schedule=schedule)
+    elif mode == "easycache":
         xr, _ = O.easycache_loop(lambda x, s: om.forward(x, s, text)[0], x0,
                                  ai.sigmas(cfg.n_steps),
                                  gate=O.GateParams(gate["tau_low"], gate["tau_high"],
@@ -228,8 +233,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1, help="untimed denoise loops")
     ap.add_argument("--workload", default="wan2.1-1.3b-shape")
     ap.add_argument("--n-steps", type=int, default=None, help="denoising steps per loop")
-    ap.add_argument("--signal", choices=["teacache", "easycache"], default="teacache",
+    ap.add_argument("--signal", choices=["teacache", "easycache", "dicache"], default="teacache",
                     help="drift signal under the adaptive gate")
+    ap.add_argument("--probe-blocks", type=int, default=1, help="DiCache probe depth")
     ap.add_argument("--tau-low", type=float, default=None,
                     help="default 0.05 (teacache) / 0.1 (easycache)")
     ap.add_argument("--tau-high", type=float, default=None,
@@ -308,7 +314,9 @@ def main() -> int:
         args.tau_low = 0.05 if args.signal == "teacache" else 0.1
     if args.tau_high is None:
         args.tau_high = 0.2
-    mode = "acid" if args.signal == "teacache" else "easycache"
+    mode = {"teacache": "acid", "easycache": "easycache", "dicache": "dicache"}[args.signal]
+    if mode == "dicache":
+        m.set_probe_blocks(args.probe_blocks)
     gate = dict(tau_low=args.tau_low, tau_high=args.tau_high, delta=args.delta)
 
     if args.sweep:
@@ -404,7 +412,7 @@ def main() -> int:
             x.copy_(x0)
             m.denoise_loop(x, sig, text_d, mode=mode, **gate)
             cpu = cpu_baseline_full(ai, cfg, traces[-1]["compute"], gate, threads,
-                                    x.cpu().numpy(), mode)
+                                    x.cpu().numpy(), mode, args.probe_blocks)
         else:
             cpu = cpu_baseline(ai, cfg, n_comp, N, threads)
 
@@ -426,7 +434,9 @@ def main() -> int:
                    "video_tokens": cfg.n_video, "text_tokens": cfg.n_text, "batch": 1,
                    "denoise_steps": N,
                    "gate": {"mode": "acid", "signal": args.signal, **gate,
-                            "n_warmup": 1 if mode == "acid" else 2},
+                            "n_warmup": 2 if mode == "easycache" else 1,
+                            **({"probe_blocks": args.probe_blocks} if mode == "dicache"
+                               else {})},
                    "parallelism": "single-gpu"},
         "computed_steps": n_comp,
         "schedule": "".join("C" if c else "S" for c in traces[-1]["compute"]),

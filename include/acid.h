@@ -60,11 +60,18 @@ typedef enum { ACID_F32 = 0, ACID_BF16 = 1 } acid_dtype;
  * each computed step i >= 1, signal s_i = k |x_i - x_{i-1}|_1 / |v_{i-1}|_1
  * with k of the last computed step, and a skipped step outputs
  * v_i = x_i + D with D = v - x of the last computed step (the whole model,
- * head included, is skipped).  Needs gate->n_warmup >= 2. */
+ * head included, is skipped).  Needs gate->n_warmup >= 2.
+ * DICACHE runs Algorithm 1 on DiCache's probe signal (Section 2, paragraph
+ * "DiCache"; Section 3.3): every step runs the first n_probe blocks
+ * (acid_model_set_probe_blocks, default 1) on [text; x_i]; the signal is
+ * the relative L1 change of the probe's video rows p_i against p_{i-1}; a
+ * computed step runs the remaining blocks and stores R = h_out_v - p_i, a
+ * skipped step uses h_out_v = p_i + R; head and Euler on every step. */
 typedef enum {
   ACID_MODE_NOCACHE = 0,
   ACID_MODE_ACID = 1,
-  ACID_MODE_EASYCACHE = 2
+  ACID_MODE_EASYCACHE = 2,
+  ACID_MODE_DICACHE = 3
 } acid_mode;
 
 /* Residual cache (TeaCache's reuse rule).  STORE on a computed step:
@@ -232,6 +239,11 @@ acid_status acid_gate(acid_gate_state* st, const acid_gate_params* p,
 acid_status acid_cache_apply(acid_cache_op op, const float* x_dev,
                              float* h_out_dev, float* r_dev, int64_t n,
                              hipStream_t stream);
+
+/* DiCache probe depth for ACID_MODE_DICACHE: the first n_probe blocks
+ * (0 <= n_probe <= n_blocks; default 1) run on every step.  Model state,
+ * kept until changed. */
+acid_status acid_model_set_probe_blocks(acid_model* m, int32_t n_probe);
 
 /* L1 sums for EasyCache's signal, in one pass over n fp32 elements:
  * out_host[0] = sum |a - b| (sum |a| if b_dev is NULL), out_host[1] =

@@ -15,7 +15,8 @@ import numpy as np
 from . import _lib as _L
 from ._lib import (ACID_BF16, ACID_CACHE_APPLY, ACID_CACHE_STORE, ACID_EPI_BIAS,  # noqa: F401
                    ACID_EPI_BIAS_GELU, ACID_EPI_EULER, ACID_EPI_GATE_RESIDUAL, ACID_EPI_QKV,
-                   ACID_F32, ACID_MODE_ACID, ACID_MODE_EASYCACHE, ACID_MODE_NOCACHE,
+                   ACID_F32, ACID_MODE_ACID, ACID_MODE_DICACHE, ACID_MODE_EASYCACHE,
+                   ACID_MODE_NOCACHE,
                    KERNEL_CLASSES, AcidError,
                    TRACE_DTYPE, check, lib)
 
@@ -194,6 +195,10 @@ class Model:
                                       C.byref(s), _stream(stream)))
         return s.value
 
+    def set_probe_blocks(self, n_probe: int) -> None:
+        """DiCache probe depth (first n_probe blocks run on every step)."""
+        check(lib().acid_model_set_probe_blocks(self.h, int(n_probe)))
+
     def l1_norms(self, a, b=None, c=None, stream=None):
         """(sum |a - b| or sum |a|, sum |c| or 0) in fp64, deterministic."""
         out = (C.c_double * 2)()
@@ -206,12 +211,13 @@ class Model:
                      n_warmup: Optional[int] = None, forced_schedule=None,
                      stream=None) -> np.ndarray:
         """Runs the loop in place on x; returns the per-step trace.  mode is
-        "nocache", "acid" (TeaCache's signal) or "easycache"; n_warmup
-        defaults to 1 (2 for "easycache")."""
+        "nocache", "acid" (TeaCache's signal), "easycache" or "dicache"
+        (probe depth: set_probe_blocks); n_warmup defaults to 1 (2 for
+        "easycache")."""
         sig = np.ascontiguousarray(sigmas, dtype=np.float32)
         n = len(sig) - 1
         modes = {"acid": ACID_MODE_ACID, "nocache": ACID_MODE_NOCACHE,
-                 "easycache": ACID_MODE_EASYCACHE}
+                 "easycache": ACID_MODE_EASYCACHE, "dicache": ACID_MODE_DICACHE}
         if mode not in modes:
             raise ValueError(f"unknown mode {mode!r}")
         modec = modes[mode]

@@ -19,7 +19,7 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "acid.h")
 
 ACID_OK, ACID_ERR_INVALID_ARG, ACID_ERR_SHAPE, ACID_ERR_HIP, ACID_ERR_UNSUPPORTED = range(5)
 ACID_F32, ACID_BF16 = 0, 1
-ACID_MODE_NOCACHE, ACID_MODE_ACID, ACID_MODE_EASYCACHE = 0, 1, 2
+ACID_MODE_NOCACHE, ACID_MODE_ACID, ACID_MODE_EASYCACHE, ACID_MODE_DICACHE = 0, 1, 2, 3
 ACID_CACHE_STORE, ACID_CACHE_APPLY = 0, 1
 (ACID_EPI_BIAS, ACID_EPI_BIAS_GELU, ACID_EPI_GATE_RESIDUAL, ACID_EPI_QKV,
  ACID_EPI_EULER) = range(5)
@@ -83,6 +83,7 @@ _SIGS = {
                             C.POINTER(C.c_int32), C.POINTER(C.c_double)]),
     "acid_cache_apply": (C.c_int, [C.c_int, _P, _P, _P, C.c_int64, _P]),
     "acid_l1_norms": (C.c_int, [_P, _P, _P, _P, C.c_int64, C.POINTER(C.c_double), _P]),
+    "acid_model_set_probe_blocks": (C.c_int, [_P, C.c_int32]),
     "acid_easycache_reuse": (C.c_int, [_P, _P, _P, _P, C.c_int64, C.c_float, _P]),
     "acid_denoise_loop": (C.c_int, [_P, _P, C.POINTER(C.c_float), C.c_int32, _P, C.c_int32,
                                     C.POINTER(GateParamsC), C.POINTER(C.c_uint8),

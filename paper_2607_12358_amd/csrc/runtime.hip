@@ -154,6 +154,7 @@ using namespace acid;
 struct acid_model {
   acid_dit_config cfg;
   int max_steps;
+  int probe_blocks = 1;  // DiCache probe depth
   char* wb;  // weight arena
   char* ws;  // workspace
   WeightLayout wl;
@@ -318,11 +319,11 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
 }
 
 // h = [text; x], all blocks with the modulation row `row`.
-acid_status stack_forward(acid_model* m, const float* row, const float* x, const float* text,
-                          hipStream_t s) {
+// h_in = [text; x] into the residual-stream buffer.
+acid_status stack_assemble(acid_model* m, const float* x, const float* text, hipStream_t s) {
   const int H = m->H();
   float* h = m->kp(m->kl.h);
-  ACID_TRY(run(m, ACID_K_MISC, s, "assemble residual stream", [&]() {
+  return run(m, ACID_K_MISC, s, "assemble residual stream", [&]() {
     hipError_t err = hipSuccess;
     if (m->Lt() > 0)
       err = hipMemcpyAsync(h, text, (size_t)m->Lt() * H * 4, hipMemcpyDeviceToDevice, s);
@@ -330,10 +331,21 @@ acid_status stack_forward(acid_model* m, const float* row, const float* x, const
       err = hipMemcpyAsync(h + m->Lt() * H, x, (size_t)m->Lv() * H * 4, hipMemcpyDeviceToDevice,
                            s);
     return err;
-  }));
-  for (int b = 0; b < m->cfg.n_blocks; ++b)
-    ACID_TRY(block_forward(m, b, row + 6 * (int64_t)b * H, h, s));
+  });
+}
+
+// Blocks [b0, b1) on the residual-stream buffer.
+acid_status stack_blocks(acid_model* m, const float* row, int b0, int b1, hipStream_t s) {
+  float* h = m->kp(m->kl.h);
+  for (int b = b0; b < b1; ++b)
+    ACID_TRY(block_forward(m, b, row + 6 * (int64_t)b * m->H(), h, s));
   return ACID_OK;
+}
+
+acid_status stack_forward(acid_model* m, const float* row, const float* x, const float* text,
+                          hipStream_t s) {
+  ACID_TRY(stack_assemble(m, x, text, s));
+  return stack_blocks(m, row, 0, m->cfg.n_blocks, s);
 }
 
 // v = LN-modulated head of h_v; EULER variant updates x in place.
@@ -446,6 +458,65 @@ acid_status easycache_loop(acid_model* m, float* x, const float* sig, int n, con
         return launch_easycache_reuse(x, xprev, v, offset, nv, dsig, s);
       }));
     }
+    cur ^= 1;
+    if (trace) {
+      trace[i].compute = compute;
+      trace[i].gate_compute = gate_compute;
+      trace[i].s = si;
+      trace[i].sigma_sum_after = st.sigma_sum;
+      trace[i].tau_used = tau;
+    }
+  }
+  return ACID_OK;
+}
+
+// DiCache's probe signal under Algorithm 1 (see acid_mode): the TEMNI
+// buffers hold the probe's video rows of this and the previous step
+// (ping-pong), the residual buffer the deep residual R = h_out_v - p.
+acid_status dicache_loop(acid_model* m, float* x, const float* sig, int n, const float* text,
+                         const acid_gate_params* gate, const uint8_t* forced,
+                         acid_step_trace* trace, hipStream_t s) {
+  const int H = m->H();
+  const int64_t nv = m->Lv() * H;
+  const int np = m->probe_blocks;
+  float* table = m->kp(m->kl.modtab);
+  float* pbuf[2] = {m->kp(m->kl.m0), m->kp(m->kl.m1)};
+  float* rdeep = m->kp(m->kl.r);
+  float* hv = m->kp(m->kl.h) + m->Lt() * H;
+  ACID_TRY(modulation_table(m, sig, n, table, s));
+  acid_gate_state st = {};
+  bool have_r = false;
+  int cur = 0;
+  for (int i = 0; i < n; ++i) {
+    const float* row = table + (int64_t)i * m->rowsz();
+    ACID_TRY(stack_assemble(m, x, text, s));
+    ACID_TRY(stack_blocks(m, row, 0, np, s));
+    float* p = pbuf[cur];
+    ACID_TRY(run(m, ACID_K_MISC, s, "keep probe features", [&]() {
+      return hipMemcpyAsync(p, hv, nv * sizeof(float), hipMemcpyDeviceToDevice, s);
+    }));
+    double si = NAN, tau = NAN;
+    if (i > 0) {
+      double sums[2];
+      ACID_TRY(l1_norms(m, p, pbuf[cur ^ 1], pbuf[cur ^ 1], nv, sums, s));
+      si = ratio_or_inf(sums[0], sums[1]);
+    }
+    int32_t gate_compute = 1;
+    ACID_TRY(acid_gate(&st, gate, si, &gate_compute, &tau));
+    const int compute = forced ? (forced[i] != 0) : gate_compute;
+    if (compute) {
+      ACID_TRY(stack_blocks(m, row, np, m->cfg.n_blocks, s));
+      ACID_TRY(run(m, ACID_K_CACHE, s, "deep residual store", [&]() {
+        return launch_cache(ACID_CACHE_STORE, p, hv, rdeep, nv, s);  // R = h_out_v - p
+      }));
+      have_r = true;
+    } else {
+      if (!have_r) return set_error(ACID_ERR_INVALID_ARG, "skip before any computed step");
+      ACID_TRY(run(m, ACID_K_CACHE, s, "deep residual apply", [&]() {
+        return launch_cache(ACID_CACHE_APPLY, p, hv, rdeep, nv, s);  // h_out_v = p + R
+      }));
+    }
+    ACID_TRY(head_forward(m, row, hv, nullptr, x, sig[i + 1] - sig[i], s));
     cur ^= 1;
     if (trace) {
       trace[i].compute = compute;
@@ -706,6 +777,15 @@ acid_status acid_block_forward(acid_model* m, int32_t block, const float* mod6_d
   return block_forward(m, block, mod6_dev, h_dev, stream);
 }
 
+acid_status acid_model_set_probe_blocks(acid_model* m, int32_t n_probe) {
+  if (!m) return set_error(ACID_ERR_INVALID_ARG, "NULL model");
+  if (n_probe < 0 || n_probe > m->cfg.n_blocks)
+    return set_error(ACID_ERR_INVALID_ARG, "n_probe %d outside [0, n_blocks=%d]", n_probe,
+                     m->cfg.n_blocks);
+  m->probe_blocks = n_probe;
+  return ACID_OK;
+}
+
 acid_status acid_l1_norms(acid_model* m, const float* a_dev, const float* b_dev,
                           const float* c_dev, int64_t n, double* out_host, hipStream_t stream) {
   if (!m || !a_dev || !out_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
@@ -783,7 +863,8 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev, const float* sigmas_h
                               const acid_gate_params* gate, const uint8_t* forced,
                               acid_step_trace* trace, hipStream_t stream) {
   if (!m || !x_dev || !sigmas_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
-  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID && mode != ACID_MODE_EASYCACHE)
+  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID && mode != ACID_MODE_EASYCACHE &&
+      mode != ACID_MODE_DICACHE)
     return set_error(ACID_ERR_INVALID_ARG, "bad mode %d", mode);
   if (mode != ACID_MODE_NOCACHE && !gate)
     return set_error(ACID_ERR_INVALID_ARG, "gate params NULL");
@@ -802,6 +883,8 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev, const float* sigmas_h
 
   if (mode == ACID_MODE_EASYCACHE)
     return easycache_loop(m, x_dev, sigmas_host, n_steps, text_dev, gate, forced, trace, stream);
+  if (mode == ACID_MODE_DICACHE)
+    return dicache_loop(m, x_dev, sigmas_host, n_steps, text_dev, gate, forced, trace, stream);
 
   const int H = m->H();
   const int64_t nv = m->Lv() * H;
