@@ -14,7 +14,9 @@
 //   into LDS in a permuted order so the matching A operand is one 16-byte
 //   read from an XOR-swizzled V^T tile (no LDS bank conflicts).  Each wave
 //   runs a two-stage software pipeline (exponentials of one tile under the
-//   score MFMAs of the next, the next tile's row max under the P V MFMAs).
+//   score MFMAs of the next; for d = 128 the next tile's row max under the
+//   P V MFMAs, for d = 64 an optimistic softmax without a row max, checked
+//   through the probability sum).
 //   Work items are mapped so each XCD streams a contiguous, head-major range
 //   (a head's K/V passes through few L2s).  Softmax runs in the exp2 domain
 //   with log2(e)/sqrt(d) folded into one FMA per score, in fp32; the row sum
@@ -238,14 +240,31 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
       }
   };
+  // Row max of the first (raw) score tile, shared with the partner half-wave
+  // that holds the other keys of the same query: the initial reference m.
+  auto first_max = [&](const f32x16(&s)[2]) {
+    float mx = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+    m_run = half_swap_max(mx) * scale_log2;
+  };
+  // Scores to exp2 arguments in place: s log2(e)/sqrt(d) - m.
+  auto shift = [&](f32x16(&s)[2]) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = __builtin_fmaf(s[kb][r], scale_log2, -m_run);
+  };
   // Row max of a raw score tile (scale > 0 commutes with max), shared with
   // the partner half-wave that holds the other keys of the same query, then
   // the tile is rewritten in place as s log2(e)/sqrt(d) - m (exp2 argument).
   // Lazy rescaling: the reference max m moves only when the new max exceeds
   // it by more than 2^8 in probability, so probabilities stay <= 256 (exact
   // range for bf16 and fp32) and the O / l rescale is skipped on most tiles.
-  float m_nx, a_nx;
-  bool g_nx;
+  float m_nx = 0.f, a_nx = 1.f;
+  bool g_nx = false;
   auto row_max_shift = [&](f32x16(&s)[2]) {
     float mx = s[0][0];
 #pragma unroll
@@ -264,7 +283,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   };
   // p = 2^(shifted score), rounded to bf16 as the B operand of the P V
   // MFMAs; the row sum adds exactly those bf16 values (v_dot2 with (1, 1)).
-  auto probs = [&](const f32x16(&s)[2], bf16x8(&pf)[2][2]) {
+  auto probs = [&](const f32x16(&s)[2], bf16x8(&pf)[2][2], float& psum) {
     const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
     float ps[2] = {0.f, 0.f};
 #pragma unroll
@@ -282,7 +301,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         }
         pf[kb][k2] = __builtin_bit_cast(bf16x8, w);
       }
-    l_run += ps[0] + ps[1];
+    psum = ps[0] + ps[1];
   };
   // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
   // (kb, k2) is S^T row kb*32 + 16 k2 + 8 (e/4) + 4 lg + e%4, i.e. key
@@ -307,39 +326,101 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   const int has_tail = (Li % BKV) != 0;
   // One pipeline iteration: sc holds S of processed tile it; S of tile it+1
   // goes to sn (on the last tile this reads a stale buffer and is dropped).
+  // One pipeline iteration: sc holds the exp2 arguments of processed tile
+  // it (against the reference m); S of tile it+1 goes to sn (on the last
+  // tile this reads a stale buffer and is dropped).
+  //
+  // d = 128 (MFMA-bound): the row max of S_{it+1} and its shift run under
+  // the P V MFMAs, and the lazy rescale is decided at the top of the next
+  // iteration.  d = 64 (VALU-bound: half the MFMA work per score):
+  // optimistic softmax, no row max.  The probabilities are formed against
+  // the current reference; a lane whose bf16 sum stays <= 2^8 had every
+  // p <= 2^8 (the lazy bound).  Otherwise (rare) the wave takes the true row
+  // max of the shifted tile, moves the reference to it, rescales O and l,
+  // and forms the probabilities again.
+  constexpr bool kOptimistic = D == 64;
   auto iter = [&](f32x16(&sc)[2], f32x16(&sn)[2], int it) {
     if (it + 2 < nkv) stage_k_dma(it & 1, (it + 2 - has_tail) * BKV);
     if (it + 1 < nkv) stage_v_dma((it + 1) & 1, (it + 1 - has_tail) * BKV);
     __builtin_amdgcn_sched_barrier(0);
-    m_run = m_nx;
-    if (__any(g_nx)) {
-      l_run *= a_nx;
+    if constexpr (!kOptimistic) {
+      m_run = m_nx;
+      if (__any(g_nx)) {
+        l_run *= a_nx;
 #pragma unroll
-      for (int db = 0; db < ND; ++db)
+        for (int db = 0; db < ND; ++db)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[db][r] *= a_nx;
+          for (int r = 0; r < 16; ++r) o[db][r] *= a_nx;
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_barrier(0);
     bf16x8 pf[2][2];
-    probs(sc, pf);
+    float psum;
+    probs(sc, pf, psum);
     scores(sn, (it + 1) & 1);
-    pv(pf, it & 1);
-    row_max_shift(sn);
-    // Interleave: each score MFMA with one fragment read and a share of the
-    // exponentials, then each P V MFMA with one read and a share of the row
-    // max and shift of the next tile.
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    if constexpr (kOptimistic) {
+      // Each score MFMA with one fragment read and a share of the
+      // exponentials.
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-    for (int i = 0; i < 2 * NK; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, (66 + 2 * NK - 1) / (2 * NK), 0);
-    }
+      for (int i = 0; i < 2 * NK; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, (66 + 2 * NK - 1) / (2 * NK), 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (__any(!(psum <= 256.0f))) {
+        float mx = sc[0][0];
 #pragma unroll
-    for (int i = 0; i < 4 * ND; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, (56 + 4 * ND - 1) / (4 * ND), 0);
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
+        mx = half_swap_max(mx);
+        const float d = mx > 0.0f ? mx : 0.0f;
+        const float alpha = __builtin_amdgcn_exp2f(-d);
+        m_run += d;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < ND; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sc[kb][r] -= d;
+        probs(sc, pf, psum);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      l_run += psum;
+      pv(pf, it & 1);
+      shift(sn);
+      // Each P V MFMA with one fragment read and a share of the shift.
+#pragma unroll
+      for (int i = 0; i < 4 * ND; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, (32 + 4 * ND - 1) / (4 * ND), 0);
+      }
+    } else {
+      l_run += psum;
+      pv(pf, it & 1);
+      row_max_shift(sn);
+      // Each score MFMA with one fragment read and a share of the
+      // exponentials, then each P V MFMA with one read and a share of the
+      // row max and shift of the next tile.
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+      for (int i = 0; i < 2 * NK; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, (66 + 2 * NK - 1) / (2 * NK), 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 4 * ND; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, (56 + 4 * ND - 1) / (4 * ND), 0);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);  // this iteration's staging has landed
@@ -369,7 +450,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         if (key >= Li) sa[kb][r] = -__builtin_inff();
       }
   }
-  row_max_shift(sa);
+  if constexpr (kOptimistic) {
+    first_max(sa);
+    shift(sa);
+  } else {
+    row_max_shift(sa);
+  }
   int it = 0;
   for (; it + 1 < nkv; it += 2) {
     iter(sa, sb, it);

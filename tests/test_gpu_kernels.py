@@ -109,6 +109,31 @@ def test_attention_f32(P, L, d):
         assert rel_err(o[:, j * d:(j + 1) * d], O.attention(q[j], k[j], v[j])) < 1e-5
 
 
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("L", [300, 1000])
+def test_attention_growing_and_spiking_scores(P, d, L):
+    """Scores that grow along the key axis (the reference max must move on
+    later tiles, by far more than the lazy bound) and one key whose score
+    dwarfs all others (a probability that would overflow without a rescale)."""
+    rng = np.random.default_rng(L + d)
+    nh = 2
+    q = bf16_values(rng.normal(size=(nh, L, d)).astype(np.float32))
+    k = rng.normal(size=(nh, L, d)).astype(np.float32)
+    k *= (1.0 + 6.0 * np.arange(L) / L)[None, :, None]
+    k[1, L // 2] = 40.0 * q[1].mean(0)
+    k = bf16_values(k)
+    v = bf16_values(rng.normal(size=(nh, L, d)).astype(np.float32))
+    vt_ld = ((L + 7) // 8) * 8
+    vt = np.zeros((nh, d, vt_ld), np.float32)
+    vt[:, :, :L] = v.transpose(0, 2, 1)
+    o = torch.empty((L, nh * d), dtype=torch.bfloat16, device="cuda")
+    P.attention(to_dev(q, torch.bfloat16), to_dev(k, torch.bfloat16), to_dev(vt, torch.bfloat16), o)
+    got = to_np(o)
+    assert np.all(np.isfinite(got))
+    for j in range(nh):
+        assert rel_err(got[:, j * d:(j + 1) * d], O.attention(q[j], k[j], v[j])) < 1e-2
+
+
 def test_attention_uniform_and_single_key(P):
     """Q = 0 gives the mean of V; L = 1 returns V (properties at any size)."""
     for L in (1, 777):
