@@ -210,7 +210,10 @@ def run_sweep(args, m, cfg, x0, text_d, sig, mode: str = "acid") -> int:
         sv = [float(v) for v in tr["s"] if math.isfinite(v)]
         ds = [abs(a - b) for a, b in zip(sv[1:], sv[:-1])]
         run = {"mode": kind, "tau_low": lo, "tau_high": hi, "delta": delta,
-               "computed_steps": n_comp, "s_per_loop": t, "speedup_vs_nocache": t_ref / t,
+               "loop": args.loop,
+        "host_loop_s_per_loop": other if graph else s_per_loop,
+        "graph_loop_s_per_loop": s_per_loop if graph else other,
+        "computed_steps": n_comp, "s_per_loop": t, "speedup_vs_nocache": t_ref / t,
                "psnr_db": psnr(x, ref),
                "steps_tau_high": int(sum(1 for v in tr["tau_used"][1:] if v == hi)),
                "drift_s_min_max": [min(sv), max(sv)] if sv else None,
@@ -241,6 +244,12 @@ def main() -> int:
     ap.add_argument("--tau-high", type=float, default=None,
                     help="default 0.2 (both signals)")
     ap.add_argument("--delta", type=float, default=0.01)
+    ap.add_argument("--loop", choices=["host", "graph"], default="host",
+                    help="host: gate on the host, one drift read-back per step; graph: gate on "
+                         "the device, the loop captured once as a HIP graph and replayed "
+                         "(teacache signal)")
+    ap.add_argument("--no-graph-context", action="store_true",
+                    help="skip timing the other loop variant as context")
     ap.add_argument("--no-nocache", action="store_true", help="skip the uncached context loop")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="disable the per-kernel event timer")
@@ -321,31 +330,62 @@ def main() -> int:
 
     if args.sweep:
         return run_sweep(args, m, cfg, x0, text_d, sig, mode)
+    if args.loop == "graph" and mode != "acid":
+        print("--loop graph runs the teacache signal (the device gate's input)", file=sys.stderr)
+        return 2
+    graph = args.loop == "graph"
+
+    def loops(count, use_graph, timed_kernels, label):
+        """count loops back to back; returns (seconds per loop, traces, timing)."""
+        if timed_kernels:
+            m.reset_timing()
+            m.set_timing(True)
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        trs = []
+        for k in range(count):
+            x.copy_(x0)
+            if use_graph:
+                # the captured loop returns without waiting; one trace suffices
+                tr = m.denoise_loop(x, sig, text_d, mode=mode, **gate, graph=True,
+                                    trace=(k == count - 1))
+            else:
+                tr = m.denoise_loop(x, sig, text_d, mode=mode, **gate)
+            if tr is not None:
+                trs.append(tr)
+            log(f"{label} loop {k} issued")
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t_start
+        tim = m.timing() if timed_kernels else {}
+        m.set_timing(False)
+        return el / count, trs, tim
 
     for w in range(args.warmup):
         x.copy_(x0)
-        tr = m.denoise_loop(x, sig, text_d, mode=mode, **gate)
+        tr = m.denoise_loop(x, sig, text_d, mode=mode, **gate, graph=graph)
         torch.cuda.synchronize()
         log(f"warmup loop {w} done: {int(tr['compute'].sum())}/{N} computed")
 
-    if not args.no_timing:
-        m.reset_timing()
-        m.set_timing(True)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    traces = []
-    for k in range(args.steps):
-        x.copy_(x0)
-        traces.append(m.denoise_loop(x, sig, text_d, mode=mode, **gate))
-        log(f"timed loop {k} issued")
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    timing = m.timing() if not args.no_timing else {}
-    m.set_timing(False)
-    s_per_loop = elapsed / args.steps
+    s_per_loop, traces, timing = loops(args.steps, graph, not args.no_timing and not graph,
+                                       "timed")
+    if graph and not args.no_timing:
+        # the event timer does not see kernels inside a graph: the per-kernel
+        # table comes from one host-gated loop (same kernels, same schedule)
+        _, host_tr, timing = loops(1, False, True, "kernel-table")
+        assert np.array_equal(host_tr[0]["compute"], traces[-1]["compute"])
+        kernel_loops = 1
+    else:
+        kernel_loops = args.steps
     n_comp = int(traces[-1]["compute"].sum())
     assert all(np.array_equal(t["compute"], traces[0]["compute"]) for t in traces)
-    log(f"{args.steps} loops in {elapsed:.3f} s -> {s_per_loop:.3f} s/loop, {n_comp}/{N} computed")
+    log(f"{args.steps} loops ({args.loop}) -> {s_per_loop:.4f} s/loop, {n_comp}/{N} computed")
+
+    other = None
+    if mode == "acid" and not args.no_graph_context:
+        x.copy_(x0)
+        m.denoise_loop(x, sig, text_d, mode=mode, **gate, graph=not graph)  # warm / capture
+        other, _, _ = loops(args.steps, not graph, False, "context")
+        log(f"context: {'host' if graph else 'graph'} loop {other:.4f} s/loop")
 
     # per-kernel-class rates over the timed region
     work = work_per_class(cfg, n_comp, N)
@@ -353,11 +393,11 @@ def main() -> int:
     for name, (ms, launches) in timing.items():
         if launches == 0:
             continue
-        ent = {"ms_per_loop": ms / args.steps, "launches_per_loop": launches / args.steps,
+        ent = {"ms_per_loop": ms / kernel_loops, "launches_per_loop": launches / kernel_loops,
                "avg_us": 1e3 * ms / launches}
         if name in work:
             kind, amount = work[name]
-            rate = amount * args.steps / (ms * 1e-3)
+            rate = amount * kernel_loops / (ms * 1e-3)
             if kind == "flop":
                 ent["tflops"] = rate / 1e12
                 if cfg.dtype == "bf16":
@@ -370,7 +410,7 @@ def main() -> int:
         kernels[name] = ent
     gemm_ms = sum(timing[k][0] for k in timing if k.startswith("gemm_"))
     gemm_flop = sum(work[k][1] for k in work if k.startswith("gemm_"))
-    gemm_tflops = gemm_flop * args.steps / (gemm_ms * 1e-3) / 1e12 if gemm_ms else None
+    gemm_tflops = gemm_flop * kernel_loops / (gemm_ms * 1e-3) / 1e12 if gemm_ms else None
 
     roofline = None
     if "attention" in kernels:
@@ -392,10 +432,13 @@ def main() -> int:
 
     nocache = None
     if not args.no_nocache:
+        if graph:  # capture first, time a replay
+            x.copy_(x0)
+            m.denoise_loop(x, sig, text_d, mode="nocache", graph=True, trace=False)
         x.copy_(x0)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        m.denoise_loop(x, sig, text_d, mode="nocache")
+        m.denoise_loop(x, sig, text_d, mode="nocache", graph=graph)
         torch.cuda.synchronize()
         nocache = time.perf_counter() - t1
         log(f"uncached loop: {nocache:.3f} s ({N} computed steps)")
@@ -438,6 +481,9 @@ def main() -> int:
                             **({"probe_blocks": args.probe_blocks} if mode == "dicache"
                                else {})},
                    "parallelism": "single-gpu"},
+        "loop": args.loop,
+        "host_loop_s_per_loop": other if graph else s_per_loop,
+        "graph_loop_s_per_loop": s_per_loop if graph else other,
         "computed_steps": n_comp,
         "schedule": "".join("C" if c else "S" for c in traces[-1]["compute"]),
         "gemm_tflops": gemm_tflops,

@@ -282,6 +282,39 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev,
                               const uint8_t* forced_schedule_host,
                               acid_step_trace* trace_host, hipStream_t stream);
 
+/* The same loop with the gate on the device and no host round trip between
+ * steps (Section 3.3's gate and the loop of Algorithm 1; the gate's low cost
+ * is the paper's claim, Section 3.2).  NOCACHE and ACID modes only
+ * (ACID_ERR_UNSUPPORTED otherwise); arguments, results and trace as
+ * acid_denoise_loop, to the bit.  Per ACID step a one-thread kernel runs the
+ * gate step on the drift the reduction left in device memory and writes the
+ * decision into a device trace; every model kernel of the step reads that
+ * word and exits at once when it is 0, and the cache kernel takes STORE or
+ * APPLY from it.  The modulation table is computed on `stream` first; the
+ * per-step launches are captured once into a HIP graph (on a stream the
+ * model owns) and replayed on `stream` by later calls with the same x_dev,
+ * text_dev, n_steps, sigmas, mode, gate and forced schedule; any change
+ * captures anew.  Without trace_host the call returns without waiting for
+ * the GPU; with it, it synchronises `stream` once at the end.  The kernel
+ * timer (acid_model_set_timing) does not see the graph's kernels. */
+acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev,
+                                    const float* sigmas_host, int32_t n_steps,
+                                    const float* text_dev, int32_t mode,
+                                    const acid_gate_params* gate,
+                                    const uint8_t* forced_schedule_host,
+                                    acid_step_trace* trace_host,
+                                    hipStream_t stream);
+
+/* Algorithm 1 (Section 3.3) on the device, one thread, over n signals
+ * s_dev[0..n) (fp64, device; NaN where a step has no signal) from the
+ * initial state: trace_dev[i] (device, n entries) as acid_gate would fill
+ * it step by step (compute == gate_compute).  The step is the same
+ * IEEE-double code as acid_gate's.  Asynchronous on `stream`. */
+acid_status acid_gate_device_sequence(const acid_gate_params* gate,
+                                      const double* s_dev, int32_t n,
+                                      acid_step_trace* trace_dev,
+                                      hipStream_t stream);
+
 /* -------------------------------------------- component calls (kernels) */
 
 /* Timestep embedding and adaLN modulation table (one row per noise level):

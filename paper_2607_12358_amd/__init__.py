@@ -20,7 +20,7 @@ from ._lib import (ACID_BF16, ACID_CACHE_APPLY, ACID_CACHE_STORE, ACID_EPI_BIAS,
                    KERNEL_CLASSES, AcidError,
                    TRACE_DTYPE, check, lib)
 
-__all__ = ["Model", "gate", "GateState", "cache_apply", "easycache_reuse", "attention", "linear",
+__all__ = ["Model", "gate", "GateState", "gate_device_sequence", "cache_apply", "easycache_reuse", "attention", "linear",
            "ln_modulate", "version", "AcidError", "KERNEL_CLASSES"]
 
 
@@ -72,6 +72,29 @@ def gate(state: GateState, tau_low: float, tau_high: float, delta: float, s_t: f
     tau = C.c_double()
     check(lib().acid_gate(C.byref(state.c), C.byref(p), float(s_t), C.byref(comp), C.byref(tau)))
     return bool(comp.value), tau.value
+
+
+def gate_device_sequence(signals, tau_low: float, tau_high: float, delta: float,
+                         n_warmup: int = 1, device="cuda", stream=None) -> np.ndarray:
+    """Algorithm 1 run by the device gate over a whole signal sequence (NaN
+    where a step has no signal); returns the trace (waits for the GPU)."""
+    torch = _torch()
+    sig = np.ascontiguousarray(signals, dtype=np.float64)
+    n = len(sig)
+    p = _L.GateParamsC(tau_low, tau_high, delta, n_warmup)
+    s_d = torch.from_numpy(sig).to(device)
+    tsz = C.sizeof(_L.StepTraceC)
+    tr_d = torch.zeros(max(n, 1) * tsz, dtype=torch.uint8, device=device)
+    check(lib().acid_gate_device_sequence(C.byref(p), _ptr(s_d), n, _ptr(tr_d),
+                                          _stream(stream)))
+    raw = tr_d.cpu().numpy()  # waits for the stream
+    tr = (_L.StepTraceC * max(n, 1))()
+    C.memmove(tr, raw.ctypes.data, max(n, 1) * tsz)
+    out = np.zeros(n, dtype=TRACE_DTYPE)
+    for i in range(n):
+        out[i] = (tr[i].compute, tr[i].gate_compute, tr[i].s, tr[i].sigma_sum_after,
+                  tr[i].tau_used)
+    return out
 
 
 # ------------------------------------------------------------ components
@@ -209,11 +232,14 @@ class Model:
     def denoise_loop(self, x, sigmas: Sequence[float], text=None, mode: str = "acid",
                      tau_low: float = 0.05, tau_high: float = 0.2, delta: float = 0.01,
                      n_warmup: Optional[int] = None, forced_schedule=None,
-                     stream=None) -> np.ndarray:
+                     stream=None, graph: bool = False,
+                     trace: bool = True) -> Optional[np.ndarray]:
         """Runs the loop in place on x; returns the per-step trace.  mode is
         "nocache", "acid" (TeaCache's signal), "easycache" or "dicache"
         (probe depth: set_probe_blocks); n_warmup defaults to 1 (2 for
-        "easycache")."""
+        "easycache").  graph=True runs the device-gate loop captured as a
+        HIP graph ("nocache" and "acid"); with trace=False it returns None
+        without waiting for the GPU."""
         sig = np.ascontiguousarray(sigmas, dtype=np.float32)
         n = len(sig) - 1
         modes = {"acid": ACID_MODE_ACID, "nocache": ACID_MODE_NOCACHE,
@@ -229,9 +255,11 @@ class Model:
         if forced_schedule is not None:
             fs = np.ascontiguousarray(forced_schedule, dtype=np.uint8)
             forced = fs.ctypes.data_as(C.POINTER(C.c_uint8))
-        check(lib().acid_denoise_loop(self.h, _ptr(x), sig.ctypes.data_as(C.POINTER(C.c_float)),
-                                      n, _ptr(text), modec, C.byref(p), forced, tr,
-                                      _stream(stream)))
+        fn = lib().acid_denoise_loop_graph if graph else lib().acid_denoise_loop
+        check(fn(self.h, _ptr(x), sig.ctypes.data_as(C.POINTER(C.c_float)), n, _ptr(text),
+                 modec, C.byref(p), forced, tr if trace else None, _stream(stream)))
+        if not trace:
+            return None
         out = np.zeros(n, dtype=TRACE_DTYPE)
         for i in range(n):
             out[i] = (tr[i].compute, tr[i].gate_compute, tr[i].s, tr[i].sigma_sum_after,

@@ -88,6 +88,10 @@ _SIGS = {
     "acid_denoise_loop": (C.c_int, [_P, _P, C.POINTER(C.c_float), C.c_int32, _P, C.c_int32,
                                     C.POINTER(GateParamsC), C.POINTER(C.c_uint8),
                                     C.POINTER(StepTraceC), _P]),
+    "acid_denoise_loop_graph": (C.c_int, [_P, _P, C.POINTER(C.c_float), C.c_int32, _P,
+                                          C.c_int32, C.POINTER(GateParamsC),
+                                          C.POINTER(C.c_uint8), C.POINTER(StepTraceC), _P]),
+    "acid_gate_device_sequence": (C.c_int, [C.POINTER(GateParamsC), _P, C.c_int32, _P, _P]),
     "acid_timestep_modulation": (C.c_int, [_P, C.POINTER(C.c_float), C.c_int32, _P, _P]),
     "acid_ln_modulate": (C.c_int, [C.c_int32, _P, C.c_int64, C.c_int32, _P, _P, _P, _P]),
     "acid_attention": (C.c_int, [C.c_int32, C.c_int32, C.c_int64, C.c_int32, _P, _P, _P,

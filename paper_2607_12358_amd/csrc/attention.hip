@@ -113,7 +113,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
                                                            const bf16* Vt,
                                                            int64_t L, int64_t vt_ld, int n_heads,
                                                            bf16* __restrict__ O,
-                                                           float scale_log2) {
+                                                           float scale_log2,
+                                                           const int32_t* pred) {
+  if (pred && *pred == 0) return;  // predicated off by the device gate
   using Ld = AttnLds<D>;
   constexpr int BQ = 32 * NW, NT = 64 * NW;  // queries / threads per workgroup
   constexpr int KLD = Ld::KLD, VLD = Ld::VLD;
@@ -488,7 +490,9 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
                                                       const float* __restrict__ Kp,
                                                       const float* __restrict__ Vt, int64_t L,
                                                       int64_t vt_ld, int n_heads,
-                                                      float* __restrict__ O, float scale) {
+                                                      float* __restrict__ O, float scale,
+                                                      const int32_t* pred) {
+  if (pred && *pred == 0) return;
   __shared__ float Ks[FKV][D];
   __shared__ float Vs[FKV][D + 1];
   const int head = blockIdx.y;
@@ -551,7 +555,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 // 4 for d = 64 (finer grid for the shorter sequences of that configuration).
 template <int D>
 hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
-                       int64_t vt_ld, void* o, hipStream_t s) {
+                       int64_t vt_ld, void* o, hipStream_t s, const int32_t* pred) {
   constexpr int NW = D == 128 ? 8 : 4;
   constexpr int BQ = 32 * NW;
   static bool attr_set = false;
@@ -566,17 +570,17 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
   dim3 grid((unsigned)(((L + BQ - 1) / BQ) * n_heads));
   hipLaunchKernelGGL((attn_bf16_kernel<D, NW>), grid, dim3(64 * NW), AttnLds<D>::BYTES, s,
                      (const bf16*)q, (const bf16*)k, (const bf16*)vt, L, vt_ld, n_heads,
-                     (bf16*)o, scale_log2);
+                     (bf16*)o, scale_log2, pred);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
-                      int64_t vt_ld, void* o, hipStream_t s) {
+                      int64_t vt_ld, void* o, hipStream_t s, const int32_t* pred) {
   dim3 grid((unsigned)((L + FQ - 1) / FQ), (unsigned)n_heads);
   hipLaunchKernelGGL(attn_f32_kernel<D>, grid, dim3(64), 0, s, (const float*)q,
                      (const float*)k, (const float*)vt, L, vt_ld, n_heads, (float*)o,
-                     1.0f / sqrtf((float)D));
+                     1.0f / sqrtf((float)D), pred);
   return hipGetLastError();
 }
 
@@ -584,14 +588,14 @@ hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, cons
 
 hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
                             const void* k, const void* vt, int64_t vt_ld, void* o,
-                            hipStream_t s) {
+                            hipStream_t s, const int32_t* pred) {
   if (L == 0) return hipSuccess;
   if (dtype == ACID_BF16) {
-    if (d == 64) return launch_bf16<64>(n_heads, L, q, k, vt, vt_ld, o, s);
-    if (d == 128) return launch_bf16<128>(n_heads, L, q, k, vt, vt_ld, o, s);
+    if (d == 64) return launch_bf16<64>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
+    if (d == 128) return launch_bf16<128>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
   } else {
-    if (d == 64) return launch_f32<64>(n_heads, L, q, k, vt, vt_ld, o, s);
-    if (d == 128) return launch_f32<128>(n_heads, L, q, k, vt, vt_ld, o, s);
+    if (d == 64) return launch_f32<64>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
+    if (d == 128) return launch_f32<128>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
   }
   return hipErrorInvalidValue;
 }

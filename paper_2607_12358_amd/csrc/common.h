@@ -68,9 +68,11 @@ inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 // Each returns hipGetLastError() of its launch.
 
 // Elementwise / row kernels (elementwise.hip)
+// A kernel given a predicate `pred` (a device int32) does nothing when
+// *pred == 0: the device-resident gate's skip decision.
 hipError_t launch_ln_modulate(int out_dtype, const float* x, int64_t rows, int H,
                               const float* shift, const float* scale, void* out,
-                              hipStream_t s);
+                              hipStream_t s, const int32_t* pred = nullptr);
 // TEMNI + per-row partial sums; m_prev may be null (then no partials).
 hipError_t launch_temni_drift(const float* x, int64_t rows, int H, const float* shift,
                               const float* scale, const float* m_prev, float* m_cur,
@@ -78,8 +80,19 @@ hipError_t launch_temni_drift(const float* x, int64_t rows, int H, const float* 
 // Fixed-order reduction of per-row (num, den) pairs -> out[0]=num, out[1]=den, out[2]=s.
 hipError_t launch_drift_finalize(const double* partials, int64_t rows, double* out,
                                  hipStream_t s);
+// With `flag` (a device int32) the operation is STORE if *flag, else APPLY.
 hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n,
-                        hipStream_t s);
+                        hipStream_t s, const int32_t* flag = nullptr);
+// dst = src (n floats, 16-byte aligned) unless predicated off.
+hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s,
+                       const int32_t* pred);
+// One step of Algorithm 1 on the device; see gate_step_kernel.
+hipError_t launch_gate_step(const double* res, int has_signal, const acid_gate_params& p,
+                            int forced, int step_index, acid_gate_state* st,
+                            acid_step_trace* tr, hipStream_t s);
+// Algorithm 1 over a signal sequence on the device.
+hipError_t launch_gate_sequence(const double* sig, int n, const acid_gate_params& p,
+                                acid_step_trace* tr, hipStream_t s);
 // fp32 [in][out] -> [out][in] in dtype
 hipError_t launch_l1_norms(const float* a, const float* b, const float* c, int64_t n,
                            double* partials, int max_groups, double* out, hipStream_t s);
@@ -101,11 +114,12 @@ hipError_t launch_skinny_gemm(const float* X, int ldx, int S, int K, const float
 
 // GEMMs (gemm.hip)
 hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, const void* wt,
-                         const acid_epilogue_args& epi, hipStream_t s);
+                         const acid_epilogue_args& epi, hipStream_t s,
+                         const int32_t* pred = nullptr);
 
 // Attention (attention.hip)
 hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
                             const void* k, const void* vt, int64_t vt_ld, void* o,
-                            hipStream_t s);
+                            hipStream_t s, const int32_t* pred = nullptr);
 
 }  // namespace acid

@@ -7,6 +7,7 @@
 // take two in-register passes (mean, then centred variance) and each row is
 // read from HBM exactly once.
 #include "common.h"
+#include "gate_step.h"
 
 namespace acid {
 
@@ -63,7 +64,9 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
                                                           int64_t rows, int H,
                                                           const float* __restrict__ shift,
                                                           const float* __restrict__ scale,
-                                                          OutT* __restrict__ out) {
+                                                          OutT* __restrict__ out,
+                                                          const int32_t* __restrict__ pred) {
+  if (pred && *pred == 0) return;  // predicated off by the device gate
   const int64_t row = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;  // whole wave leaves together
@@ -169,9 +172,8 @@ __global__ __launch_bounds__(1024) void drift_finalize_kernel(const double* __re
 
 // STORE: r = h - x ; APPLY: h = x + r.  float4 body, scalar tail.
 template <int OP>
-__global__ __launch_bounds__(256) void cache_kernel(const float* __restrict__ x,
-                                                    float* __restrict__ h,
-                                                    float* __restrict__ r, int64_t n) {
+__device__ __forceinline__ void cache_body(const float* __restrict__ x, float* __restrict__ h,
+                                           float* __restrict__ r, int64_t n) {
   const int64_t n4 = n >> 2;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const float4* x4 = reinterpret_cast<const float4*>(x);
@@ -193,6 +195,95 @@ __global__ __launch_bounds__(256) void cache_kernel(const float* __restrict__ x,
       r[i] = h[i] - x[i];
     else
       h[i] = x[i] + r[i];
+  }
+}
+
+template <int OP>
+__global__ __launch_bounds__(256) void cache_kernel(const float* __restrict__ x,
+                                                    float* __restrict__ h,
+                                                    float* __restrict__ r, int64_t n) {
+  cache_body<OP>(x, h, r, n);
+}
+
+// The operation chosen by the device gate's decision: STORE after a computed
+// step, APPLY on a skipped one.
+__global__ __launch_bounds__(256) void cache_by_flag_kernel(const float* __restrict__ x,
+                                                            float* __restrict__ h,
+                                                            float* __restrict__ r, int64_t n,
+                                                            const int32_t* __restrict__ flag) {
+  if (*flag)
+    cache_body<ACID_CACHE_STORE>(x, h, r, n);
+  else
+    cache_body<ACID_CACHE_APPLY>(x, h, r, n);
+}
+
+// dst = src over n floats (16-byte aligned), unless the device gate's flag
+// says skip.
+__global__ __launch_bounds__(256) void copy_pred_kernel(const float* __restrict__ src,
+                                                        float* __restrict__ dst, int64_t n,
+                                                        const int32_t* __restrict__ pred) {
+  if (pred && *pred == 0) return;
+  const int64_t n4 = n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const float4* s4 = reinterpret_cast<const float4*>(src);
+  float4* d4 = reinterpret_cast<float4*>(dst);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride)
+    d4[i] = s4[i];
+  if (blockIdx.x == 0 && threadIdx.x < (n & 3)) dst[n4 * 4 + threadIdx.x] = src[n4 * 4 + threadIdx.x];
+}
+
+// Device-resident gate, one step of Algorithm 1 per launch (one thread).
+// The signal is res[2] (the drift reduction's output) when has_signal, else
+// NaN.  step_index 0 starts from the initial state.  The decision goes to
+// tr->compute (the predicate of the step's model kernels): the gate's own,
+// or forced (0/1) when forced >= 0.
+__global__ void gate_step_kernel(const double* __restrict__ res, int has_signal,
+                                 acid_gate_params p, int forced, int step_index,
+                                 acid_gate_state* __restrict__ st,
+                                 acid_step_trace* __restrict__ tr) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  acid_gate_state g;
+  if (step_index == 0) {
+    g.sigma_sum = 0.0;
+    g.s_prev = 0.0;
+    g.has_prev = 0;
+    g.step = 0;
+  } else {
+    g = *st;
+  }
+  const double s = has_signal ? res[2] : __builtin_nan("");
+  double tau;
+  const int32_t c = gate_step(&g, &p, s, &tau);
+  *st = g;
+  acid_step_trace t;
+  t.compute = forced >= 0 ? forced : c;
+  t.gate_compute = c;
+  t.s = s;
+  t.sigma_sum_after = g.sigma_sum;
+  t.tau_used = tau;
+  *tr = t;
+}
+
+// Algorithm 1 over a whole signal sequence s[0..n) on the device (one thread),
+// for checking the device gate against the host gate and the worked example.
+__global__ void gate_sequence_kernel(const double* __restrict__ s, int n, acid_gate_params p,
+                                     acid_step_trace* __restrict__ tr) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  acid_gate_state g;
+  g.sigma_sum = 0.0;
+  g.s_prev = 0.0;
+  g.has_prev = 0;
+  g.step = 0;
+  for (int i = 0; i < n; ++i) {
+    double tau;
+    const int32_t c = gate_step(&g, &p, s[i], &tau);
+    acid_step_trace t;
+    t.compute = c;
+    t.gate_compute = c;
+    t.s = s[i];
+    t.sigma_sum_after = g.sigma_sum;
+    t.tau_used = tau;
+    tr[i] = t;
   }
 }
 
@@ -352,12 +443,12 @@ static int row_chunks(int H) {
 
 hipError_t launch_ln_modulate(int out_dtype, const float* x, int64_t rows, int H,
                               const float* shift, const float* scale, void* out,
-                              hipStream_t s) {
+                              hipStream_t s, const int32_t* pred) {
   if (rows == 0) return hipSuccess;
   const int cpl = row_chunks(H);
   dim3 grid((unsigned)((rows + kRowsPerBlock - 1) / kRowsPerBlock));
-#define LN_BF(C) hipLaunchKernelGGL((ln_modulate_kernel<C, bf16>), grid, dim3(256), 0, s, x, rows, H, shift, scale, (bf16*)out)
-#define LN_F(C) hipLaunchKernelGGL((ln_modulate_kernel<C, float>), grid, dim3(256), 0, s, x, rows, H, shift, scale, (float*)out)
+#define LN_BF(C) hipLaunchKernelGGL((ln_modulate_kernel<C, bf16>), grid, dim3(256), 0, s, x, rows, H, shift, scale, (bf16*)out, pred)
+#define LN_F(C) hipLaunchKernelGGL((ln_modulate_kernel<C, float>), grid, dim3(256), 0, s, x, rows, H, shift, scale, (float*)out, pred)
   if (out_dtype == ACID_BF16) {
     ACID_ROW_DISPATCH(cpl, LN_BF)
   } else {
@@ -386,12 +477,19 @@ hipError_t launch_drift_finalize(const double* partials, int64_t rows, double* o
   return hipGetLastError();
 }
 
-hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  int64_t n4 = (n + 3) / 4;
-  int64_t blocks = (n4 + 255) / 256;
+static unsigned stream_grid(int64_t n) {
+  int64_t blocks = ((n + 3) / 4 + 255) / 256;
   if (blocks > 256 * 16) blocks = 256 * 16;
-  if (op == ACID_CACHE_STORE)
+  return (unsigned)blocks;
+}
+
+hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n, hipStream_t s,
+                        const int32_t* flag) {
+  if (n == 0) return hipSuccess;
+  const unsigned blocks = stream_grid(n);
+  if (flag)
+    hipLaunchKernelGGL(cache_by_flag_kernel, dim3(blocks), dim3(256), 0, s, x, h, r, n, flag);
+  else if (op == ACID_CACHE_STORE)
     hipLaunchKernelGGL(cache_kernel<ACID_CACHE_STORE>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
   else
     hipLaunchKernelGGL(cache_kernel<ACID_CACHE_APPLY>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
@@ -404,6 +502,28 @@ static int l1_grid(int64_t n, int max_groups) {
   if (g > 1024) g = 1024;
   if (g > max_groups) g = max_groups;
   return (int)g;
+}
+
+hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s,
+                       const int32_t* pred) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_pred_kernel, dim3(stream_grid(n)), dim3(256), 0, s, src, dst, n, pred);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_step(const double* res, int has_signal, const acid_gate_params& p,
+                            int forced, int step_index, acid_gate_state* st,
+                            acid_step_trace* tr, hipStream_t s) {
+  hipLaunchKernelGGL(gate_step_kernel, dim3(1), dim3(64), 0, s, res, has_signal, p, forced,
+                     step_index, st, tr);
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_sequence(const double* sig, int n, const acid_gate_params& p,
+                                acid_step_trace* tr, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(gate_sequence_kernel, dim3(1), dim3(64), 0, s, sig, n, p, tr);
+  return hipGetLastError();
 }
 
 hipError_t launch_l1_norms(const float* a, const float* b, const float* c, int64_t n,

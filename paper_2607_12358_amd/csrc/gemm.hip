@@ -41,6 +41,7 @@ struct Epi {
   int64_t M;
   int n_heads, head_dim, H;
   float dsigma;
+  const int32_t* pred;  // device gate's decision: no work when *pred == 0
 };
 
 template <int KIND, typename T>
@@ -213,6 +214,7 @@ template <int KIND>
 __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A, const bf16* Wt,
                                                                    int64_t M, int N, int K,
                                                                    Epi e) {
+  if (e.pred && *e.pred == 0) return;
   // Two stages of A and B tiles, one LDS object per tile so the compiler can
   // tell the stage being read from the stage being filled.
   __shared__ __attribute__((aligned(1024))) bf16 As0[kTileElems], Bs0[kTileElems];
@@ -415,6 +417,7 @@ template <int KIND>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A,
                                                        const float* __restrict__ Wt, int64_t M,
                                                        int N, int K, Epi e) {
+  if (e.pred && *e.pred == 0) return;
   __shared__ float As[16][64 + 4];
   __shared__ float Ws[16][64 + 4];
   const int64_t m0 = (int64_t)blockIdx.x * 64;
@@ -476,7 +479,7 @@ hipError_t launch_kind(int dtype, int64_t M, int N, int K, const void* a, const 
 }  // namespace
 
 hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, const void* wt,
-                         const acid_epilogue_args& ea, hipStream_t s) {
+                         const acid_epilogue_args& ea, hipStream_t s, const int32_t* pred) {
   if (M == 0) return hipSuccess;
   Epi e;
   e.bias = ea.bias;
@@ -492,6 +495,7 @@ hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, cons
   e.head_dim = ea.head_dim;
   e.H = ea.n_heads * ea.head_dim;
   e.dsigma = ea.dsigma;
+  e.pred = pred;
   switch (ea.kind) {
     case ACID_EPI_BIAS: return launch_kind<ACID_EPI_BIAS>(dtype, M, N, K, a, wt, e, s);
     case ACID_EPI_BIAS_GELU: return launch_kind<ACID_EPI_BIAS_GELU>(dtype, M, N, K, a, wt, e, s);

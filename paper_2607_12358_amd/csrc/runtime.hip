@@ -109,6 +109,7 @@ WeightLayout weight_layout(const acid_dit_config& c) {
 
 struct WorkLayout {
   size_t h, act, q, k, vt, o, g, modtab, temb_e, temb_hid, temb_u, partials, dres, m0, m1, r, v;
+  size_t dtrace, gstate;  // device-resident gate: per-step trace, state
   size_t total;
   int64_t vt_ld;
 };
@@ -142,6 +143,8 @@ WorkLayout work_layout(const acid_dit_config& c, int max_steps) {
   W.m1 = put(Lv * H * 4);
   W.r = put(Lv * H * 4);
   W.v = put(Lv * H * 4);
+  W.dtrace = put(S * sizeof(acid_step_trace));
+  W.gstate = put(sizeof(acid_gate_state));
   W.total = off;
   return W;
 }
@@ -169,6 +172,25 @@ struct acid_model {
   std::vector<hipEvent_t> pool;
   double total_ms[ACID_K_COUNT] = {};
   int64_t launches[ACID_K_COUNT] = {};
+  // captured loop (device-resident gate): the executable graph, the stream
+  // it was captured on, and what it was captured for
+  bool capturing = false;
+  hipStream_t cap = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  struct GraphKey {
+    float* x = nullptr;
+    const float* text = nullptr;
+    int n = 0, mode = -1;
+    acid_gate_params gate = {};
+    std::vector<float> sigmas;
+    std::vector<uint8_t> forced;
+    bool operator==(const GraphKey& o) const {
+      return x == o.x && text == o.text && n == o.n && mode == o.mode &&
+             gate.tau_low == o.gate.tau_low && gate.tau_high == o.gate.tau_high &&
+             gate.delta == o.gate.delta && gate.n_warmup == o.gate.n_warmup &&
+             sigmas == o.sigmas && forced == o.forced;
+    }
+  } gkey;
 
   int H() const { return cfg.hidden; }
   int64_t Lv() const { return cfg.n_video; }
@@ -213,7 +235,8 @@ acid_status get_event(acid_model* m, hipEvent_t* e) {
 template <class F>
 acid_status run(acid_model* m, int cls, hipStream_t s, const char* what, F&& f) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (m->timing) {
+  const bool timed = m->timing && !m->capturing;  // no timer inside a captured graph
+  if (timed) {
     if (m->pending.size() > 4096) ACID_TRY(harvest(m));
     ACID_TRY(get_event(m, &e0));
     ACID_TRY(get_event(m, &e1));
@@ -221,7 +244,7 @@ acid_status run(acid_model* m, int cls, hipStream_t s, const char* what, F&& f) 
   }
   hipError_t err = f();
   if (err != hipSuccess) return check_hip(err, what);
-  if (m->timing) {
+  if (timed) {
     ACID_HIP(hipEventRecord(e1, s));
     m->pending.push_back({cls, e0, e1});
   }
@@ -259,13 +282,15 @@ acid_status modulation_table(acid_model* m, const float* sigmas, int n, float* t
 }
 
 acid_status ln_mod(acid_model* m, const float* x, int64_t rows, const float* shift,
-                   const float* scale, void* out, hipStream_t s) {
+                   const float* scale, void* out, hipStream_t s, const int32_t* pred = nullptr) {
   return run(m, ACID_K_LN_MOD, s, "ln_modulate", [&]() {
-    return launch_ln_modulate(m->cfg.dtype, x, rows, m->H(), shift, scale, out, s);
+    return launch_ln_modulate(m->cfg.dtype, x, rows, m->H(), shift, scale, out, s, pred);
   });
 }
 
-acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hipStream_t s) {
+// pred: the device gate's decision word (null: unconditional).
+acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hipStream_t s,
+                          const int32_t* pred = nullptr) {
   const acid_dit_config& c = m->cfg;
   const int H = c.hidden, F = c.ffn;
   const int64_t L = m->L();
@@ -274,7 +299,7 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   void* g = m->kp<void>(m->kl.g);
   const int dt = c.dtype;
 
-  ACID_TRY(ln_mod(m, h, L, mod6, mod6 + H, act, s));
+  ACID_TRY(ln_mod(m, h, L, mod6, mod6 + H, act, s, pred));
 
   acid_epilogue_args e = {};
   e.kind = ACID_EPI_QKV;
@@ -286,10 +311,10 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   e.n_heads = c.n_heads;
   e.head_dim = c.head_dim;
   ACID_TRY(run(m, ACID_K_GEMM_QKV, s, "qkv gemm", [&]() {
-    return launch_linear(dt, L, 3 * H, H, act, m->bp<void>(b, m->wl.qkv_w), e, s);
+    return launch_linear(dt, L, 3 * H, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred);
   }));
   ACID_TRY(run(m, ACID_K_ATTENTION, s, "attention", [&]() {
-    return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, o, s);
+    return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, o, s, pred);
   }));
   acid_epilogue_args p = {};
   p.kind = ACID_EPI_GATE_RESIDUAL;
@@ -297,15 +322,15 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   p.gate = mod6 + 2 * H;
   p.out = h;
   ACID_TRY(run(m, ACID_K_GEMM_PROJ, s, "proj gemm", [&]() {
-    return launch_linear(dt, L, H, H, o, m->bp<void>(b, m->wl.o_w), p, s);
+    return launch_linear(dt, L, H, H, o, m->bp<void>(b, m->wl.o_w), p, s, pred);
   }));
-  ACID_TRY(ln_mod(m, h, L, mod6 + 3 * H, mod6 + 4 * H, act, s));
+  ACID_TRY(ln_mod(m, h, L, mod6 + 3 * H, mod6 + 4 * H, act, s, pred));
   acid_epilogue_args f1 = {};
   f1.kind = ACID_EPI_BIAS_GELU;
   f1.bias = m->bp(b, m->wl.f1_b);
   f1.out = g;
   ACID_TRY(run(m, ACID_K_GEMM_FFN1, s, "ffn1 gemm", [&]() {
-    return launch_linear(dt, L, F, H, act, m->bp<void>(b, m->wl.f1_w), f1, s);
+    return launch_linear(dt, L, F, H, act, m->bp<void>(b, m->wl.f1_w), f1, s, pred);
   }));
   acid_epilogue_args f2 = {};
   f2.kind = ACID_EPI_GATE_RESIDUAL;
@@ -313,7 +338,7 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   f2.gate = mod6 + 5 * H;
   f2.out = h;
   ACID_TRY(run(m, ACID_K_GEMM_FFN2, s, "ffn2 gemm", [&]() {
-    return launch_linear(dt, L, H, F, g, m->bp<void>(b, m->wl.f2_w), f2, s);
+    return launch_linear(dt, L, H, F, g, m->bp<void>(b, m->wl.f2_w), f2, s, pred);
   }));
   return ACID_OK;
 }
@@ -335,11 +360,26 @@ acid_status stack_assemble(acid_model* m, const float* x, const float* text, hip
 }
 
 // Blocks [b0, b1) on the residual-stream buffer.
-acid_status stack_blocks(acid_model* m, const float* row, int b0, int b1, hipStream_t s) {
+acid_status stack_blocks(acid_model* m, const float* row, int b0, int b1, hipStream_t s,
+                         const int32_t* pred = nullptr) {
   float* h = m->kp(m->kl.h);
   for (int b = b0; b < b1; ++b)
-    ACID_TRY(block_forward(m, b, row + 6 * (int64_t)b * m->H(), h, s));
+    ACID_TRY(block_forward(m, b, row + 6 * (int64_t)b * m->H(), h, s, pred));
   return ACID_OK;
+}
+
+// stack_assemble as predicated copy kernels (graph capture: no copy nodes
+// that would run on skipped steps).
+acid_status stack_assemble_pred(acid_model* m, const float* x, const float* text,
+                                const int32_t* pred, hipStream_t s) {
+  const int H = m->H();
+  float* h = m->kp(m->kl.h);
+  return run(m, ACID_K_MISC, s, "assemble residual stream", [&]() {
+    hipError_t err = hipSuccess;
+    if (m->Lt() > 0) err = launch_copy(text, h, m->Lt() * H, s, pred);
+    if (err == hipSuccess) err = launch_copy(x, h + m->Lt() * H, m->Lv() * H, s, pred);
+    return err;
+  });
 }
 
 acid_status stack_forward(acid_model* m, const float* row, const float* x, const float* text,
@@ -529,6 +569,72 @@ acid_status dicache_loop(acid_model* m, float* x, const float* sig, int n, const
   return ACID_OK;
 }
 
+acid_status check_loop_args(acid_model* m, float* x_dev, const float* sigmas_host,
+                            int32_t n_steps, const float* text_dev, int32_t mode,
+                            const acid_gate_params* gate, const uint8_t* forced) {
+  if (!m || !x_dev || !sigmas_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID && mode != ACID_MODE_EASYCACHE &&
+      mode != ACID_MODE_DICACHE)
+    return set_error(ACID_ERR_INVALID_ARG, "bad mode %d", mode);
+  if (mode != ACID_MODE_NOCACHE && !gate)
+    return set_error(ACID_ERR_INVALID_ARG, "gate params NULL");
+  if (mode == ACID_MODE_EASYCACHE && gate->n_warmup < 2)
+    return set_error(ACID_ERR_INVALID_ARG, "EasyCache needs n_warmup >= 2 (got %d)",
+                     gate->n_warmup);
+  if (n_steps < 1 || n_steps > m->max_steps)
+    return set_error(ACID_ERR_INVALID_ARG, "n_steps %d must be in [1, max_steps=%d]", n_steps,
+                     m->max_steps);
+  if ((m->cfg.n_text > 0) != (text_dev != nullptr))
+    return set_error(ACID_ERR_INVALID_ARG, "text must be given iff n_text > 0");
+  if (forced && !forced[0])
+    return set_error(ACID_ERR_INVALID_ARG, "forced schedule must compute step 0");
+  if (forced && mode == ACID_MODE_NOCACHE)
+    return set_error(ACID_ERR_UNSUPPORTED, "a forced schedule needs ACID mode (the residual cache)");
+  return ACID_OK;
+}
+
+// The whole loop as one stream of launches with no host round trip: per
+// step the drift, the device gate (which writes the step's decision into the
+// device trace), the model kernels predicated on that decision, the cache
+// kernel taking STORE or APPLY from it, and the head + Euler update.
+acid_status enqueue_device_gate_loop(acid_model* m, float* x, const float* sig, int n,
+                                     const float* text, int mode, const acid_gate_params* gate,
+                                     const uint8_t* forced, hipStream_t s) {
+  const int H = m->H();
+  const int64_t nv = m->Lv() * H;
+  const float* table = m->kp(m->kl.modtab);
+  float* mbuf[2] = {m->kp(m->kl.m0), m->kp(m->kl.m1)};
+  float* r = m->kp(m->kl.r);
+  float* hv = m->kp(m->kl.h) + m->Lt() * H;
+  const double* dres = m->kp<double>(m->kl.dres);
+  acid_step_trace* dtr = m->kp<acid_step_trace>(m->kl.dtrace);
+  acid_gate_state* gst = m->kp<acid_gate_state>(m->kl.gstate);
+  int cur = 0;
+  for (int i = 0; i < n; ++i) {
+    const float* row = table + (int64_t)i * m->rowsz();
+    const int32_t* pred = nullptr;
+    if (mode == ACID_MODE_ACID) {
+      const float* mprev = i > 0 ? mbuf[cur ^ 1] : nullptr;
+      ACID_TRY(drift(m, row, x, mprev, mbuf[cur], s));
+      cur ^= 1;
+      const int f = forced ? (forced[i] != 0) : -1;
+      ACID_TRY(run(m, ACID_K_DRIFT, s, "device gate", [&]() {
+        return launch_gate_step(dres, i > 0, *gate, f, i, gst, dtr + i, s);
+      }));
+      pred = &dtr[i].compute;
+    }
+    ACID_TRY(stack_assemble_pred(m, x, text, pred, s));
+    ACID_TRY(stack_blocks(m, row, 0, m->cfg.n_blocks, s, pred));
+    if (mode == ACID_MODE_ACID) {
+      ACID_TRY(run(m, ACID_K_CACHE, s, "cache store/apply", [&]() {
+        return launch_cache(ACID_CACHE_STORE, x, hv, r, nv, s, pred);
+      }));
+    }
+    ACID_TRY(head_forward(m, row, hv, nullptr, x, sig[i + 1] - sig[i], s));
+  }
+  return ACID_OK;
+}
+
 acid_status read_drift(acid_model* m, double* s_out, hipStream_t s) {
   double res[3];
   ACID_HIP(hipMemcpyAsync(res, m->kp<double>(m->kl.dres), sizeof res, hipMemcpyDeviceToHost, s));
@@ -667,6 +773,8 @@ void acid_model_destroy(acid_model* m) {
   if (!m) return;
   harvest(m);
   for (auto e : m->pool) hipEventDestroy(e);
+  if (m->gexec) hipGraphExecDestroy(m->gexec);
+  if (m->cap) hipStreamDestroy(m->cap);
   delete m;
 }
 
@@ -862,24 +970,7 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev, const float* sigmas_h
                               int32_t n_steps, const float* text_dev, int32_t mode,
                               const acid_gate_params* gate, const uint8_t* forced,
                               acid_step_trace* trace, hipStream_t stream) {
-  if (!m || !x_dev || !sigmas_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
-  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID && mode != ACID_MODE_EASYCACHE &&
-      mode != ACID_MODE_DICACHE)
-    return set_error(ACID_ERR_INVALID_ARG, "bad mode %d", mode);
-  if (mode != ACID_MODE_NOCACHE && !gate)
-    return set_error(ACID_ERR_INVALID_ARG, "gate params NULL");
-  if (mode == ACID_MODE_EASYCACHE && gate->n_warmup < 2)
-    return set_error(ACID_ERR_INVALID_ARG, "EasyCache needs n_warmup >= 2 (got %d)",
-                     gate->n_warmup);
-  if (n_steps < 1 || n_steps > m->max_steps)
-    return set_error(ACID_ERR_INVALID_ARG, "n_steps %d must be in [1, max_steps=%d]", n_steps,
-                     m->max_steps);
-  if ((m->cfg.n_text > 0) != (text_dev != nullptr))
-    return set_error(ACID_ERR_INVALID_ARG, "text must be given iff n_text > 0");
-  if (forced && !forced[0])
-    return set_error(ACID_ERR_INVALID_ARG, "forced schedule must compute step 0");
-  if (forced && mode == ACID_MODE_NOCACHE)
-    return set_error(ACID_ERR_UNSUPPORTED, "a forced schedule needs ACID mode (the residual cache)");
+  ACID_TRY(check_loop_args(m, x_dev, sigmas_host, n_steps, text_dev, mode, gate, forced));
 
   if (mode == ACID_MODE_EASYCACHE)
     return easycache_loop(m, x_dev, sigmas_host, n_steps, text_dev, gate, forced, trace, stream);
@@ -931,6 +1022,77 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev, const float* sigmas_h
     }
   }
   return ACID_OK;
+}
+
+acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev, const float* sigmas_host,
+                                    int32_t n_steps, const float* text_dev, int32_t mode,
+                                    const acid_gate_params* gate, const uint8_t* forced,
+                                    acid_step_trace* trace, hipStream_t stream) {
+  ACID_TRY(check_loop_args(m, x_dev, sigmas_host, n_steps, text_dev, mode, gate, forced));
+  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID)
+    return set_error(ACID_ERR_UNSUPPORTED,
+                     "the captured loop supports the NOCACHE and ACID modes (got %d)", mode);
+  ACID_TRY(modulation_table(m, sigmas_host, n_steps, m->kp(m->kl.modtab), stream));
+
+  acid_model::GraphKey key;
+  key.x = x_dev;
+  key.text = text_dev;
+  key.n = n_steps;
+  key.mode = mode;
+  if (gate) key.gate = *gate;
+  key.sigmas.assign(sigmas_host, sigmas_host + n_steps + 1);
+  if (forced) key.forced.assign(forced, forced + n_steps);
+  if (!m->gexec || !(key == m->gkey)) {
+    if (m->gexec) {
+      ACID_HIP(hipGraphExecDestroy(m->gexec));
+      m->gexec = nullptr;
+    }
+    if (!m->cap) ACID_HIP(hipStreamCreateWithFlags(&m->cap, hipStreamNonBlocking));
+    ACID_HIP(hipStreamBeginCapture(m->cap, hipStreamCaptureModeRelaxed));
+    m->capturing = true;
+    const acid_status st = enqueue_device_gate_loop(m, x_dev, sigmas_host, n_steps, text_dev,
+                                                    mode, gate, forced, m->cap);
+    m->capturing = false;
+    hipGraph_t g = nullptr;
+    const hipError_t e = hipStreamEndCapture(m->cap, &g);
+    if (st != ACID_OK || e != hipSuccess) {
+      if (g) hipGraphDestroy(g);
+      return st != ACID_OK ? st : check_hip(e, "hipStreamEndCapture");
+    }
+    const hipError_t ei = hipGraphInstantiate(&m->gexec, g, nullptr, nullptr, 0);
+    hipGraphDestroy(g);
+    if (ei != hipSuccess) {
+      m->gexec = nullptr;
+      return check_hip(ei, "hipGraphInstantiate");
+    }
+    m->gkey = key;
+  }
+  ACID_HIP(hipGraphLaunch(m->gexec, stream));
+  if (trace) {
+    if (mode == ACID_MODE_ACID) {
+      ACID_HIP(hipMemcpyAsync(trace, m->kp(m->kl.dtrace), n_steps * sizeof(acid_step_trace),
+                              hipMemcpyDeviceToHost, stream));
+      ACID_HIP(hipStreamSynchronize(stream));
+    } else {
+      for (int i = 0; i < n_steps; ++i) {
+        trace[i].compute = 1;
+        trace[i].gate_compute = 1;
+        trace[i].s = NAN;
+        trace[i].sigma_sum_after = 0.0;
+        trace[i].tau_used = NAN;
+      }
+    }
+  }
+  return ACID_OK;
+}
+
+acid_status acid_gate_device_sequence(const acid_gate_params* gate, const double* s_dev,
+                                      int32_t n, acid_step_trace* trace_dev,
+                                      hipStream_t stream) {
+  if (!gate || n < 0 || (n > 0 && (!s_dev || !trace_dev)))
+    return set_error(ACID_ERR_INVALID_ARG, "bad gate sequence arguments");
+  const hipError_t e = launch_gate_sequence(s_dev, n, *gate, trace_dev, stream);
+  return e == hipSuccess ? ACID_OK : check_hip(e, "gate sequence");
 }
 
 }  // extern "C"

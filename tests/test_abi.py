@@ -68,6 +68,18 @@ def test_null_arguments_rejected(lib):
     assert lib.acid_cache_apply(0, None, None, None, 0, None) == 0  # empty is a no-op
 
 
+def test_device_gate_and_graph_loop_argument_errors(lib):
+    """Argument checks that return before any GPU work."""
+    pc = L.GateParamsC(0.05, 0.2, 0.01, 1)
+    assert lib.acid_gate_device_sequence(None, None, 0, None, None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_gate_device_sequence(C.byref(pc), None, 3, None, None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_gate_device_sequence(C.byref(pc), None, -1, None, None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_gate_device_sequence(C.byref(pc), None, 0, None, None) == 0  # empty: no-op
+    sig = (C.c_float * 3)(1.0, 0.5, 0.0)
+    assert lib.acid_denoise_loop_graph(None, None, sig, 2, None, 1, C.byref(pc), None, None,
+                                       None) == L.ACID_ERR_INVALID_ARG
+
+
 def _c_gate_run(lib, s_seq, p):
     st = L.GateStateC()
     pc = L.GateParamsC(p.tau_low, p.tau_high, p.delta, p.n_warmup)

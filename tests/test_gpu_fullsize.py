@@ -204,6 +204,15 @@ def test_denoise_loop_wan_fullsize_properties(P):
     x2 = x0.clone()
     tr2 = m.denoise_loop(x2, sig, mode="acid", tau_low=0.05, tau_high=0.2, delta=0.01)
     assert torch.equal(x, x2) and np.array_equal(tr["s"][1:], tr2["s"][1:])
+    # the gate on the device and the loop captured as a graph: the same bits
+    for _ in range(2):
+        xg = x0.clone()
+        trg = m.denoise_loop(xg, sig, mode="acid", tau_low=0.05, tau_high=0.2, delta=0.01,
+                             graph=True)
+        assert torch.equal(xg, x)
+        assert np.array_equal(trg["compute"], tr["compute"])
+        assert np.array_equal(trg["s"][1:], tr["s"][1:])
+        assert np.array_equal(trg["sigma_sum_after"], tr["sigma_sum_after"])
     x3 = x0.clone()
     tr3 = m.denoise_loop(x3, sig, mode="acid", tau_low=math.inf, tau_high=math.inf, delta=0.01)
     assert int(tr3["compute"].sum()) == 1 and tr3["compute"][0] == 1
@@ -238,3 +247,8 @@ def test_denoise_loop_small_bf16_vs_oracle(P):
     ok = ~np.isnan(otr["s"])
     np.testing.assert_allclose(tr["s"][ok], otr["s"][ok], rtol=2e-2)
     assert rel_err(to_np(x) - x0, xr - x0) < 2e-2
+    # the captured device-gate loop gives the same bits
+    xg = to_dev(x0)
+    trg = m.denoise_loop(xg, sig, mode="acid", tau_low=0.05, tau_high=0.2, delta=0.01,
+                         graph=True)
+    assert torch.equal(xg, x) and np.array_equal(trg["compute"], tr["compute"])
