@@ -54,6 +54,11 @@ class DiTConfig:
     freq_dim: int = 256
     dtype: str = "bf16"          # "f32" or "bf16"
     n_steps: int = 50
+    # "sequential": attention then MLP, each with its own LN-modulate and
+    # gated residual; "parallel": HunyuanVideo's single-stream form, both
+    # branches from one LN-modulate and one gated residual, reusing the same
+    # tensors as [qkv.w | ffn1.w] and [o.w ; ffn2.w].
+    block: str = "sequential"
 
     @property
     def n_tokens(self) -> int:
@@ -77,7 +82,8 @@ COG5B = DiTConfig("cogvideox-5b-shape", n_blocks=42, hidden=3072, n_heads=48,
 HUNYUAN = DiTConfig("hunyuanvideo-slice", n_blocks=4, hidden=3072, n_heads=24,
                     head_dim=128, ffn=12288, n_video=33 * 45 * 80, n_text=256,
                     n_steps=50)
-CONFIGS = {c.name: c for c in (TINY, SMALL, WAN13B, COG5B, HUNYUAN)}
+HUNYUAN_PARALLEL = HUNYUAN.replace(name="hunyuanvideo-slice-parallel", block="parallel")
+CONFIGS = {c.name: c for c in (TINY, SMALL, WAN13B, COG5B, HUNYUAN, HUNYUAN_PARALLEL)}
 
 
 def manifest(cfg: DiTConfig) -> List[Tuple[str, Tuple[int, ...]]]:

@@ -35,6 +35,13 @@ What is computed, and where it comes from
   self-attention over all tokens, a tanh-GELU MLP, and a modulated
   LayerNorm + linear head.  The reverse process (Section 3.1, eq. (2)) is
   realised as a flow-matching Euler step x_{i+1} = x_i + (s_{i+1} - s_i) v_i.
+* The parallel block (``parallel_block``) is HunyuanVideo's single-stream
+  block (HunyuanVideo is the first model of Section 4.1): attention and MLP
+  branches from one modulated LayerNorm, projected together, one gated
+  residual.  Pinned by reduction to the sequential block: equal to it when
+  the MLP weights are zero, equal to it when the attention weights are zero
+  and the second modulation triple equals the first, and its two branches
+  add.
 
 Pins
 ----
@@ -205,6 +212,8 @@ class DiTModel:
         Returns the block output for ``rows`` (all rows if None).  Keys and
         values always span all L tokens.
         """
+        if getattr(self.cfg, "block", "sequential") == "parallel":
+            return self.parallel_block(h, b, mod6, rows)
         cfg = self.cfg
         H = cfg.hidden
         shift1, scale1, gate1, shift2, scale2, gate2 = mod6
@@ -222,6 +231,40 @@ class DiTModel:
         a2 = modulate(layer_norm(hr), shift2, scale2)
         f = gelu_tanh(a2 @ self.w(pre + "ffn1.w") + self.w(pre + "ffn1.b"))
         return hr + gate2 * (f @ self.w(pre + "ffn2.w") + self.w(pre + "ffn2.b"))
+
+    def parallel_block(self, h: np.ndarray, b: int, mod6: np.ndarray,
+                       rows: Optional[np.ndarray] = None) -> np.ndarray:
+        """HunyuanVideo's single-stream block (the model Section 4.1
+        evaluates), in parallel form: one modulated LayerNorm a feeds both
+        the attention branch and the MLP branch, whose outputs are projected
+        together and added to the residual stream through one gate:
+
+            a = LN(h) (1 + scale1) + shift1
+            o = attention(a W_q + b_q, a W_k + b_k, a W_v + b_v)
+            out = h + gate1 (o W_o + b_o + gelu_tanh(a W_1 + b_1) W_2 + b_2)
+
+        i.e. linear1 = [W_qkv | W_1] (H -> 3H + F) and linear2 = [W_o ; W_2]
+        (H + F -> H) of that design, from the same tensors as the sequential
+        block; the second modulation triple is unused.
+        """
+        cfg = self.cfg
+        H = cfg.hidden
+        shift1, scale1, gate1 = mod6[0], mod6[1], mod6[2]
+        h = np.asarray(h, dtype=F64)
+        pre = f"blocks.{b}."
+        a = modulate(layer_norm(h), shift1, scale1)
+        wqkv, bqkv = self.w(pre + "qkv.w"), self.w(pre + "qkv.b")
+        kv = a @ wqkv[:, H:] + bqkv[H:]
+        k, v = kv[:, :H], kv[:, H:]
+        if rows is None:
+            rows = np.arange(h.shape[0])
+        ar = a[rows]
+        q = ar @ wqkv[:, :H] + bqkv[:H]
+        o = multi_head_attention(q, k, v, cfg.n_heads)
+        f = gelu_tanh(ar @ self.w(pre + "ffn1.w") + self.w(pre + "ffn1.b"))
+        y = (o @ self.w(pre + "o.w") + self.w(pre + "o.b")
+             + f @ self.w(pre + "ffn2.w") + self.w(pre + "ffn2.b"))
+        return h[rows] + gate1 * y
 
     def stack(self, x: np.ndarray, sigma: float, text: Optional[np.ndarray] = None) -> np.ndarray:
         """All blocks on h_in = [text; x]; returns the video rows h_out_v."""
