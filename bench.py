@@ -52,18 +52,27 @@ def work_per_class(cfg, n_computed: int, n_steps: int) -> dict:
     L, Lv, H, F, nb = cfg.n_tokens, cfg.n_video, cfg.hidden, cfg.ffn, cfg.n_blocks
     es = 2 if cfg.dtype == "bf16" else 4
     kc = n_computed
+    if getattr(cfg, "block", "sequential") == "parallel":
+        # [W_qkv | W_1] in one GEMM (class gemm_qkv), [W_o ; W_2] in one
+        # (class gemm_proj), one LN-modulate per block
+        gemms = {"gemm_qkv": ("flop", kc * nb * 2.0 * L * H * (3 * H + F)),
+                 "gemm_proj": ("flop", kc * nb * 2.0 * L * (H + F) * H)}
+        ln_per_block = 1
+    else:
+        gemms = {"gemm_qkv": ("flop", kc * nb * 2.0 * L * H * 3 * H),
+                 "gemm_proj": ("flop", kc * nb * 2.0 * L * H * H),
+                 "gemm_ffn1": ("flop", kc * nb * 2.0 * L * H * F),
+                 "gemm_ffn2": ("flop", kc * nb * 2.0 * L * F * H)}
+        ln_per_block = 2
     return {
         "attention": ("flop", kc * nb * 4.0 * L * L * H),
-        "gemm_qkv": ("flop", kc * nb * 2.0 * L * H * 3 * H),
-        "gemm_proj": ("flop", kc * nb * 2.0 * L * H * H),
-        "gemm_ffn1": ("flop", kc * nb * 2.0 * L * H * F),
-        "gemm_ffn2": ("flop", kc * nb * 2.0 * L * F * H),
+        **gemms,
         "gemm_head": ("flop", n_steps * 2.0 * Lv * H * H),
         # TEMNI reads x, writes m; with a previous m also reads it (all fp32)
         "drift": ("byte", (8.0 + 12.0 * (n_steps - 1)) * Lv * H),
         # store: read x, h_out; write r.  apply: read x, r; write h_out.
         "cache": ("byte", n_steps * 12.0 * Lv * H),
-        "ln_mod": ("byte", (kc * nb * 2 * L + n_steps * Lv) * H * (4.0 + es)),
+        "ln_mod": ("byte", (kc * nb * ln_per_block * L + n_steps * Lv) * H * (4.0 + es)),
     }
 
 
@@ -475,6 +484,7 @@ def main() -> int:
         "config": {"workload": cfg.name, "n_blocks": cfg.n_blocks, "hidden": cfg.hidden,
                    "heads": cfg.n_heads, "head_dim": cfg.head_dim, "ffn": cfg.ffn,
                    "video_tokens": cfg.n_video, "text_tokens": cfg.n_text, "batch": 1,
+                   "block": cfg.block,
                    "denoise_steps": N,
                    "gate": {"mode": "acid", "signal": args.signal, **gate,
                             "n_warmup": 2 if mode == "easycache" else 1,

@@ -78,6 +78,16 @@ typedef enum {
  * r = h_out - x.  APPLY on a skipped step: h_out = x + r. */
 typedef enum { ACID_CACHE_STORE = 0, ACID_CACHE_APPLY = 1 } acid_cache_op;
 
+/* Block form.  SEQUENTIAL: LN-modulate, attention, gated projection into
+ * the residual stream, LN-modulate, GELU MLP, gated projection (shift/scale/
+ * gate 1 and 2).  PARALLEL: HunyuanVideo's single-stream block (the first
+ * model of Section 4.1): one LN-modulate (shift1, scale1) feeds
+ * [q | k | v | mlp] = a [W_qkv | W_1] + [b_qkv | b_1]; attention and
+ * GELU(mlp) are projected together by [W_o ; W_2] (K = H + F) and added
+ * with gate1, biases b_o + b_2; the second modulation triple is unused.
+ * Both use the same parameter manifest. */
+typedef enum { ACID_BLOCK_SEQUENTIAL = 0, ACID_BLOCK_PARALLEL = 1 } acid_block_kind;
+
 /* Shape of the DiT stack.  Token rows are ordered text first, then video.
  * hidden = n_heads * head_dim.  Supported: head_dim 64 or 128; hidden
  * (<= 4096) and ffn multiples of 128 (every GEMM's N and K); freq_dim even
@@ -92,6 +102,7 @@ typedef struct {
   int32_t n_video;  /* video tokens L_v (the latent rows) */
   int32_t n_text;   /* text tokens L_t (0 if none) */
   int32_t dtype;    /* acid_dtype */
+  int32_t block_kind; /* acid_block_kind */
 } acid_dit_config;
 
 /* Algorithm 1's parameters (its "Require" line): tau_low, tau_high and the
@@ -348,21 +359,26 @@ typedef enum {
   ACID_EPI_BIAS_GELU = 1,     /* out dtype [M][N] = GELU_tanh(y) */
   ACID_EPI_GATE_RESIDUAL = 2, /* out fp32 [M][N] += gate (.) y  (in place) */
   ACID_EPI_QKV = 3,           /* y split into Q | K | V heads (see below) */
-  ACID_EPI_EULER = 4          /* out fp32 [M][N] += dsigma * y (in place);
+  ACID_EPI_EULER = 4,         /* out fp32 [M][N] += dsigma * y (in place);
                                  v_out (optional) fp32 [M][N] = y */
+  ACID_EPI_QKV_GELU = 5       /* columns < 3 n_heads head_dim as QKV; column
+                                 3 n_heads head_dim + j (j < N - 3 H) to
+                                 out dtype [M][out_ld] at j: GELU_tanh(y) */
 } acid_epilogue;
 
 typedef struct {
   int32_t kind;         /* acid_epilogue */
   const float* bias;    /* [N], required */
   const float* gate;    /* [N], GATE_RESIDUAL only */
+  const float* bias2;   /* [N], GATE_RESIDUAL: optional second bias (NULL: none) */
   void* out;            /* see acid_epilogue */
+  int64_t out_ld;       /* QKV_GELU: row stride of out (elements) */
   float* v_out;         /* EULER only, may be NULL */
   void* q;              /* QKV: [n_heads][M][head_dim] */
   void* k;              /* QKV: [n_heads][M][head_dim] */
   void* vt;             /* QKV: [n_heads][head_dim][vt_ld] */
   int64_t vt_ld;        /* QKV: >= round_up(M, 8) */
-  int32_t n_heads;      /* QKV: N == 3 * n_heads * head_dim */
+  int32_t n_heads;      /* QKV: N == 3 * n_heads * head_dim (QKV_GELU: >) */
   int32_t head_dim;     /* QKV */
   float dsigma;         /* EULER */
 } acid_epilogue_args;

@@ -15,6 +15,7 @@ import numpy as np
 from . import _lib as _L
 from ._lib import (ACID_BF16, ACID_CACHE_APPLY, ACID_CACHE_STORE, ACID_EPI_BIAS,  # noqa: F401
                    ACID_EPI_BIAS_GELU, ACID_EPI_EULER, ACID_EPI_GATE_RESIDUAL, ACID_EPI_QKV,
+                   ACID_EPI_QKV_GELU, ACID_BLOCK_PARALLEL, ACID_BLOCK_SEQUENTIAL,
                    ACID_F32, ACID_MODE_ACID, ACID_MODE_DICACHE, ACID_MODE_EASYCACHE,
                    ACID_MODE_NOCACHE,
                    KERNEL_CLASSES, AcidError,
@@ -132,8 +133,10 @@ def attention(q, k, vt, o, stream=None) -> None:
 
 
 def linear(a, wt, kind: int, bias, gate=None, out=None, v_out=None, q=None, k=None, vt=None,
-           n_heads=0, head_dim=0, dsigma=0.0, stream=None) -> None:
-    """Fused GEMM y = a @ wt.T + bias with an epilogue (see include/acid.h)."""
+           n_heads=0, head_dim=0, dsigma=0.0, bias2=None, stream=None) -> None:
+    """Fused GEMM y = a @ wt.T + bias with an epilogue (see include/acid.h).
+    For ACID_EPI_QKV_GELU, out may be a row-strided view (unit column
+    stride); its row stride is passed as out_ld."""
     M, K = a.shape
     N = wt.shape[0]
     code = ACID_BF16 if a.dtype == _torch().bfloat16 else ACID_F32
@@ -141,7 +144,14 @@ def linear(a, wt, kind: int, bias, gate=None, out=None, v_out=None, q=None, k=No
     e.kind = kind
     e.bias = _ptr(bias)
     e.gate = _ptr(gate)
-    e.out = _ptr(out)
+    e.bias2 = _ptr(bias2)
+    if kind == _L.ACID_EPI_QKV_GELU and out is not None:
+        if not out.is_cuda or out.stride(-1) != 1:
+            raise ValueError("out must be a device tensor with unit column stride")
+        e.out = C.c_void_p(out.data_ptr())
+        e.out_ld = out.stride(0)
+    else:
+        e.out = _ptr(out)
     e.v_out = _ptr(v_out)
     e.q, e.k, e.vt = _ptr(q), _ptr(k), _ptr(vt)
     e.vt_ld = vt.shape[-1] if vt is not None else 0

@@ -22,7 +22,8 @@ ACID_F32, ACID_BF16 = 0, 1
 ACID_MODE_NOCACHE, ACID_MODE_ACID, ACID_MODE_EASYCACHE, ACID_MODE_DICACHE = 0, 1, 2, 3
 ACID_CACHE_STORE, ACID_CACHE_APPLY = 0, 1
 (ACID_EPI_BIAS, ACID_EPI_BIAS_GELU, ACID_EPI_GATE_RESIDUAL, ACID_EPI_QKV,
- ACID_EPI_EULER) = range(5)
+ ACID_EPI_EULER, ACID_EPI_QKV_GELU) = range(6)
+ACID_BLOCK_SEQUENTIAL, ACID_BLOCK_PARALLEL = 0, 1
 KERNEL_CLASSES = ("temb", "ln_mod", "gemm_qkv", "attention", "gemm_proj", "gemm_ffn1",
                   "gemm_ffn2", "gemm_head", "drift", "cache", "misc")
 
@@ -36,7 +37,8 @@ class AcidError(RuntimeError):
 class DitConfigC(C.Structure):
     _fields_ = [("n_blocks", C.c_int32), ("hidden", C.c_int32), ("n_heads", C.c_int32),
                 ("head_dim", C.c_int32), ("ffn", C.c_int32), ("freq_dim", C.c_int32),
-                ("n_video", C.c_int32), ("n_text", C.c_int32), ("dtype", C.c_int32)]
+                ("n_video", C.c_int32), ("n_text", C.c_int32), ("dtype", C.c_int32),
+                ("block_kind", C.c_int32)]
 
 
 class GateParamsC(C.Structure):
@@ -56,7 +58,8 @@ class StepTraceC(C.Structure):
 
 class EpilogueArgsC(C.Structure):
     _fields_ = [("kind", C.c_int32), ("bias", C.c_void_p), ("gate", C.c_void_p),
-                ("out", C.c_void_p), ("v_out", C.c_void_p), ("q", C.c_void_p),
+                ("bias2", C.c_void_p), ("out", C.c_void_p), ("out_ld", C.c_int64),
+                ("v_out", C.c_void_p), ("q", C.c_void_p),
                 ("k", C.c_void_p), ("vt", C.c_void_p), ("vt_ld", C.c_int64),
                 ("n_heads", C.c_int32), ("head_dim", C.c_int32), ("dsigma", C.c_float)]
 
@@ -146,8 +149,10 @@ def dtype_code(dtype) -> int:
 
 def config_c(cfg) -> DitConfigC:
     """acid_dit_config from any object with the DiT shape attributes."""
+    kind = {"sequential": ACID_BLOCK_SEQUENTIAL, "parallel": ACID_BLOCK_PARALLEL}[
+        getattr(cfg, "block", "sequential")]
     return DitConfigC(cfg.n_blocks, cfg.hidden, cfg.n_heads, cfg.head_dim, cfg.ffn,
-                      cfg.freq_dim, cfg.n_video, cfg.n_text, dtype_code(cfg.dtype))
+                      cfg.freq_dim, cfg.n_video, cfg.n_text, dtype_code(cfg.dtype), kind)
 
 
 TRACE_DTYPE = np.dtype([("compute", np.int32), ("gate_compute", np.int32), ("s", np.float64),

@@ -112,7 +112,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
                                                            const bf16* Kp,
                                                            const bf16* Vt,
                                                            int64_t L, int64_t vt_ld, int n_heads,
-                                                           bf16* __restrict__ O,
+                                                           bf16* __restrict__ O, int64_t o_ld,
                                                            float scale_log2,
                                                            const int32_t* pred) {
   if (pred && *pred == 0) return;  // predicated off by the device gate
@@ -407,10 +407,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
       l_run += psum;
       pv(pf, it & 1);
       row_max_shift(sn);
-      // Each score MFMA with one fragment read and a share of the
-      // exponentials, then each P V MFMA with one read and a share of the
-      // row max and shift of the next tile.
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      // Four fragment reads ahead, then each score MFMA with one more read
+      // and a share of the exponentials, then each P V MFMA with one read
+      // and a share of the row max and shift of the next tile.
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
       for (int i = 0; i < 2 * NK; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -468,7 +468,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
   const float inv = 1.0f / l_tot;
   if (qrow < L) {
-    bf16* orow = O + qrow * ((int64_t)n_heads * D) + (int64_t)head * D;
+    bf16* orow = O + qrow * o_ld + (int64_t)head * D;
 #pragma unroll
     for (int db = 0; db < ND; ++db)
 #pragma unroll
@@ -490,8 +490,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
                                                       const float* __restrict__ Kp,
                                                       const float* __restrict__ Vt, int64_t L,
                                                       int64_t vt_ld, int n_heads,
-                                                      float* __restrict__ O, float scale,
-                                                      const int32_t* pred) {
+                                                      float* __restrict__ O, int64_t o_ld,
+                                                      float scale, const int32_t* pred) {
   if (pred && *pred == 0) return;
   __shared__ float Ks[FKV][D];
   __shared__ float Vs[FKV][D + 1];
@@ -545,7 +545,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
   }
   if (qrow < L) {
     const float inv = 1.0f / l_run;
-    float* orow = O + qrow * ((int64_t)n_heads * D) + (int64_t)head * D;
+    float* orow = O + qrow * o_ld + (int64_t)head * D;
 #pragma unroll
     for (int d = 0; d < D; ++d) orow[d] = o[d] * inv;
   }
@@ -555,7 +555,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
 // 4 for d = 64 (finer grid for the shorter sequences of that configuration).
 template <int D>
 hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
-                       int64_t vt_ld, void* o, hipStream_t s, const int32_t* pred) {
+                       int64_t vt_ld, void* o, int64_t o_ld, hipStream_t s,
+                       const int32_t* pred) {
   constexpr int NW = D == 128 ? 8 : 4;
   constexpr int BQ = 32 * NW;
   static bool attr_set = false;
@@ -570,16 +571,16 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
   dim3 grid((unsigned)(((L + BQ - 1) / BQ) * n_heads));
   hipLaunchKernelGGL((attn_bf16_kernel<D, NW>), grid, dim3(64 * NW), AttnLds<D>::BYTES, s,
                      (const bf16*)q, (const bf16*)k, (const bf16*)vt, L, vt_ld, n_heads,
-                     (bf16*)o, scale_log2, pred);
+                     (bf16*)o, o_ld, scale_log2, pred);
   return hipGetLastError();
 }
 
 template <int D>
 hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
-                      int64_t vt_ld, void* o, hipStream_t s, const int32_t* pred) {
+                      int64_t vt_ld, void* o, int64_t o_ld, hipStream_t s, const int32_t* pred) {
   dim3 grid((unsigned)((L + FQ - 1) / FQ), (unsigned)n_heads);
   hipLaunchKernelGGL(attn_f32_kernel<D>, grid, dim3(64), 0, s, (const float*)q,
-                     (const float*)k, (const float*)vt, L, vt_ld, n_heads, (float*)o,
+                     (const float*)k, (const float*)vt, L, vt_ld, n_heads, (float*)o, o_ld,
                      1.0f / sqrtf((float)D), pred);
   return hipGetLastError();
 }
@@ -588,14 +589,15 @@ hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, cons
 
 hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
                             const void* k, const void* vt, int64_t vt_ld, void* o,
-                            hipStream_t s, const int32_t* pred) {
+                            hipStream_t s, const int32_t* pred, int64_t o_ld) {
   if (L == 0) return hipSuccess;
+  if (o_ld == 0) o_ld = (int64_t)n_heads * d;
   if (dtype == ACID_BF16) {
-    if (d == 64) return launch_bf16<64>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
-    if (d == 128) return launch_bf16<128>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
+    if (d == 64) return launch_bf16<64>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
+    if (d == 128) return launch_bf16<128>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
   } else {
-    if (d == 64) return launch_f32<64>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
-    if (d == 128) return launch_f32<128>(n_heads, L, q, k, vt, vt_ld, o, s, pred);
+    if (d == 64) return launch_f32<64>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
+    if (d == 128) return launch_f32<128>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
   }
   return hipErrorInvalidValue;
 }

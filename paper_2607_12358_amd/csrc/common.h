@@ -98,8 +98,9 @@ hipError_t launch_l1_norms(const float* a, const float* b, const float* c, int64
                            double* partials, int max_groups, double* out, hipStream_t s);
 hipError_t launch_easycache_reuse(float* x, float* xp, float* v, const float* d, int64_t n,
                                   float dsig, hipStream_t s);
+// dst row o at dst + o * ldd (ldd 0: in).
 hipError_t launch_transpose_convert(const float* src, int64_t in, int64_t out, int dtype,
-                                    void* dst, hipStream_t s);
+                                    void* dst, hipStream_t s, int64_t ldd = 0);
 
 // Timestep embedding + modulation (temb.hip)
 // e[i][:] = [cos(t f_j)]_j ++ [sin(t f_j)]_j with t = 1000 sigmas_host[i], in fp64.
@@ -118,8 +119,9 @@ hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, cons
                          const int32_t* pred = nullptr);
 
 // Attention (attention.hip)
+// o_ld: row stride of O in elements (0: n_heads * d).
 hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
                             const void* k, const void* vt, int64_t vt_ld, void* o,
-                            hipStream_t s, const int32_t* pred = nullptr);
+                            hipStream_t s, const int32_t* pred = nullptr, int64_t o_ld = 0);
 
 }  // namespace acid

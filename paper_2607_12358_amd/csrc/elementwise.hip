@@ -400,7 +400,7 @@ __global__ __launch_bounds__(256) void easycache_reuse_kernel(float* __restrict_
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_convert_kernel(const float* __restrict__ src,
                                                                 int64_t nin, int64_t nout,
-                                                                T* __restrict__ dst) {
+                                                                T* __restrict__ dst, int64_t ldd) {
   __shared__ float tile[32][33];
   const int64_t o0 = (int64_t)blockIdx.x * 32, i0 = (int64_t)blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
@@ -411,7 +411,7 @@ __global__ __launch_bounds__(256) void transpose_convert_kernel(const float* __r
   __syncthreads();
   for (int k = ty; k < 32; k += 8) {
     int64_t o = o0 + k, i = i0 + tx;
-    if (o < nout && i < nin) dst[o * nin + i] = (T)tile[tx][k];
+    if (o < nout && i < nin) dst[o * ldd + i] = (T)tile[tx][k];
   }
 }
 
@@ -551,12 +551,13 @@ hipError_t launch_easycache_reuse(float* x, float* xp, float* v, const float* d,
 }
 
 hipError_t launch_transpose_convert(const float* src, int64_t nin, int64_t nout, int dtype,
-                                    void* dst, hipStream_t s) {
+                                    void* dst, hipStream_t s, int64_t ldd) {
+  if (ldd == 0) ldd = nin;
   dim3 grid((unsigned)((nout + 31) / 32), (unsigned)((nin + 31) / 32));
   if (dtype == ACID_BF16)
-    hipLaunchKernelGGL(transpose_convert_kernel<bf16>, grid, dim3(256), 0, s, src, nin, nout, (bf16*)dst);
+    hipLaunchKernelGGL(transpose_convert_kernel<bf16>, grid, dim3(256), 0, s, src, nin, nout, (bf16*)dst, ldd);
   else
-    hipLaunchKernelGGL(transpose_convert_kernel<float>, grid, dim3(256), 0, s, src, nin, nout, (float*)dst);
+    hipLaunchKernelGGL(transpose_convert_kernel<float>, grid, dim3(256), 0, s, src, nin, nout, (float*)dst, ldd);
   return hipGetLastError();
 }
 

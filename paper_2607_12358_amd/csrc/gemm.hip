@@ -42,11 +42,29 @@ struct Epi {
   int n_heads, head_dim, H;
   float dsigma;
   const int32_t* pred;  // device gate's decision: no work when *pred == 0
+  const float* bias2;   // GATE_RESIDUAL: optional second bias
+  int64_t out_ld;       // QKV_GELU: row stride of the GELU output
+  int n_qkv;            // QKV_GELU: columns [0, n_qkv) are Q | K | V
 };
+
+// Q | K | V head-major destination of column c < 3 H (which = c / H).
+template <typename T>
+__device__ __forceinline__ T* qkv_dst(const Epi& e, int c, int64_t& stride) {
+  const int which = c / e.H, cc = c - which * e.H;
+  const int head = cc / e.head_dim, dd = cc - head * e.head_dim;
+  if (which < 2) {
+    stride = e.head_dim;
+    return static_cast<T*>(which == 0 ? e.q : e.k) + (int64_t)head * e.M * e.head_dim + dd;
+  }
+  stride = 1;
+  return static_cast<T*>(e.vt) + ((int64_t)head * e.head_dim + dd) * e.vt_ld;
+}
 
 template <int KIND, typename T>
 __device__ __forceinline__ void epi_elem(const Epi& e, int64_t m, int n, int N, float acc) {
-  const float y = acc + e.bias[n];
+  float bias = e.bias[n];
+  if (KIND == ACID_EPI_GATE_RESIDUAL && e.bias2) bias += e.bias2[n];
+  const float y = acc + bias;
   const int64_t idx = m * N + n;
   if constexpr (KIND == ACID_EPI_BIAS) {
     static_cast<float*>(e.out)[idx] = y;
@@ -55,14 +73,13 @@ __device__ __forceinline__ void epi_elem(const Epi& e, int64_t m, int n, int N, 
   } else if constexpr (KIND == ACID_EPI_GATE_RESIDUAL) {
     float* h = static_cast<float*>(e.out) + idx;
     *h = *h + e.gate[n] * y;
-  } else if constexpr (KIND == ACID_EPI_QKV) {
-    const int which = n / e.H, c = n - which * e.H;
-    const int head = c / e.head_dim, dd = c - head * e.head_dim;
-    if (which < 2) {
-      T* dst = static_cast<T*>(which == 0 ? e.q : e.k);
-      dst[((int64_t)head * e.M + m) * e.head_dim + dd] = (T)y;
+  } else if constexpr (KIND == ACID_EPI_QKV || KIND == ACID_EPI_QKV_GELU) {
+    if (KIND == ACID_EPI_QKV || n < e.n_qkv) {
+      int64_t stride;
+      T* dst = qkv_dst<T>(e, n, stride);
+      dst[m * stride] = (T)y;
     } else {
-      static_cast<T*>(e.vt)[((int64_t)head * e.head_dim + dd) * e.vt_ld + m] = (T)y;
+      static_cast<T*>(e.out)[m * e.out_ld + (n - e.n_qkv)] = (T)gelu_tanh(y);
     }
   } else {  // ACID_EPI_EULER
     if (e.v_out) e.v_out[idx] = y;
@@ -81,23 +98,26 @@ struct ColEpi {
   float* v_f;
   int64_t stride;
   float dsigma;
+  bool gelu;  // QKV_GELU: this column is in the GELU part
   __device__ __forceinline__ ColEpi(const Epi& e, int n, int N) {
     bias = e.bias[n];
+    if (KIND == ACID_EPI_GATE_RESIDUAL && e.bias2) bias += e.bias2[n];
     gate = (KIND == ACID_EPI_GATE_RESIDUAL) ? e.gate[n] : 0.f;
     dsigma = e.dsigma;
     dst_t = nullptr;
     dst_f = nullptr;
     v_f = nullptr;
     stride = N;
+    gelu = false;
     if constexpr (KIND == ACID_EPI_QKV) {
-      const int which = n / e.H, c = n - which * e.H;
-      const int head = c / e.head_dim, dd = c - head * e.head_dim;
-      if (which < 2) {
-        dst_t = static_cast<T*>(which == 0 ? e.q : e.k) + (int64_t)head * e.M * e.head_dim + dd;
-        stride = e.head_dim;
+      dst_t = qkv_dst<T>(e, n, stride);
+    } else if constexpr (KIND == ACID_EPI_QKV_GELU) {
+      if (n < e.n_qkv) {
+        dst_t = qkv_dst<T>(e, n, stride);
       } else {
-        dst_t = static_cast<T*>(e.vt) + ((int64_t)head * e.head_dim + dd) * e.vt_ld;
-        stride = 1;
+        gelu = true;
+        dst_t = static_cast<T*>(e.out) + (n - e.n_qkv);
+        stride = e.out_ld;
       }
     } else if constexpr (KIND == ACID_EPI_BIAS_GELU) {
       dst_t = static_cast<T*>(e.out) + n;
@@ -137,6 +157,15 @@ struct ColEpi {
       *h = *h + gate * y;
     } else if constexpr (KIND == ACID_EPI_QKV) {
       dst_t[m * stride] = (T)y;
+    } else if constexpr (KIND == ACID_EPI_QKV_GELU) {
+      float z = y;
+      if (gelu) {
+        if constexpr (sizeof(T) == 2)
+          z = gelu_tanh_fast(y);
+        else
+          z = gelu_tanh(y);
+      }
+      dst_t[m * stride] = (T)z;
     } else {
       if (v_f) v_f[m * stride] = y;
       float* x = dst_f + m * stride;
@@ -496,6 +525,9 @@ hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, cons
   e.H = ea.n_heads * ea.head_dim;
   e.dsigma = ea.dsigma;
   e.pred = pred;
+  e.bias2 = ea.bias2;
+  e.out_ld = ea.out_ld;
+  e.n_qkv = 3 * ea.n_heads * ea.head_dim;
   switch (ea.kind) {
     case ACID_EPI_BIAS: return launch_kind<ACID_EPI_BIAS>(dtype, M, N, K, a, wt, e, s);
     case ACID_EPI_BIAS_GELU: return launch_kind<ACID_EPI_BIAS_GELU>(dtype, M, N, K, a, wt, e, s);
@@ -503,6 +535,7 @@ hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, cons
       return launch_kind<ACID_EPI_GATE_RESIDUAL>(dtype, M, N, K, a, wt, e, s);
     case ACID_EPI_QKV: return launch_kind<ACID_EPI_QKV>(dtype, M, N, K, a, wt, e, s);
     case ACID_EPI_EULER: return launch_kind<ACID_EPI_EULER>(dtype, M, N, K, a, wt, e, s);
+    case ACID_EPI_QKV_GELU: return launch_kind<ACID_EPI_QKV_GELU>(dtype, M, N, K, a, wt, e, s);
     default: return hipErrorInvalidValue;
   }
 }

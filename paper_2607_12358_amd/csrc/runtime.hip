@@ -53,6 +53,9 @@ acid_status check_config(const acid_dit_config* c) {
     return set_error(ACID_ERR_SHAPE, "ffn %d: must be a positive multiple of 128", c->ffn);
   if (c->freq_dim < 2 || c->freq_dim % 2 || c->freq_dim > 1024)
     return set_error(ACID_ERR_SHAPE, "freq_dim %d: must be even and <= 1024", c->freq_dim);
+  if (c->block_kind != ACID_BLOCK_SEQUENTIAL && c->block_kind != ACID_BLOCK_PARALLEL)
+    return set_error(ACID_ERR_INVALID_ARG, "block_kind %d is not SEQUENTIAL or PARALLEL",
+                     c->block_kind);
   return ACID_OK;
 }
 
@@ -87,15 +90,19 @@ WeightLayout weight_layout(const acid_dit_config& c) {
     b = align_up(b + bytes);
     return o;
   };
+  // With H and F multiples of 128 every size below is a multiple of the
+  // 256-byte alignment, so neighbours are contiguous: [W_qkv^T ; W_1^T] is one
+  // [3H + F][H] operand, [b_qkv | b_1] one bias, and the o_w + f2_w region
+  // holds the parallel block's [W_o ; W_2]^T as one [H][H + F] operand.
   L.ada_w = putb(H * 6 * H * 4);
   L.ada_b = putb(6 * H * 4);
   L.qkv_w = putb(3 * H * H * es);
-  L.qkv_b = putb(3 * H * 4);
-  L.o_w = putb(H * H * es);
-  L.o_b = putb(H * 4);
   L.f1_w = putb(F * H * es);
+  L.qkv_b = putb(3 * H * 4);
   L.f1_b = putb(F * 4);
+  L.o_w = putb(H * H * es);
   L.f2_w = putb(H * F * es);
+  L.o_b = putb(H * 4);
   L.f2_b = putb(H * 4);
   L.blk_stride = b;
   off += b * c.n_blocks;
@@ -132,7 +139,8 @@ WorkLayout work_layout(const acid_dit_config& c, int max_steps) {
   W.k = put(L * H * es);
   W.vt = put((size_t)c.n_heads * c.head_dim * W.vt_ld * es);
   W.o = put(L * H * es);
-  W.g = put(L * F * es);
+  // parallel block: [attention output | GELU(mlp)] rows of H + F
+  W.g = put(L * (F + (c.block_kind == ACID_BLOCK_PARALLEL ? H : 0)) * es);
   W.modtab = put(S * (6 * (size_t)c.n_blocks + 2) * H * 4);
   W.temb_e = put(S * Ft * 4);
   W.temb_hid = put(S * H * 4);
@@ -289,8 +297,12 @@ acid_status ln_mod(acid_model* m, const float* x, int64_t rows, const float* shi
 }
 
 // pred: the device gate's decision word (null: unconditional).
+acid_status block_forward_parallel(acid_model* m, int b, const float* mod6, float* h,
+                                   hipStream_t s, const int32_t* pred);
+
 acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hipStream_t s,
                           const int32_t* pred = nullptr) {
+  if (m->cfg.block_kind == ACID_BLOCK_PARALLEL) return block_forward_parallel(m, b, mod6, h, s, pred);
   const acid_dit_config& c = m->cfg;
   const int H = c.hidden, F = c.ffn;
   const int64_t L = m->L();
@@ -341,6 +353,48 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
     return launch_linear(dt, L, H, F, g, m->bp<void>(b, m->wl.f2_w), f2, s, pred);
   }));
   return ACID_OK;
+}
+
+// HunyuanVideo's single-stream block: one LN-modulate, one GEMM into
+// Q | K | V and GELU(mlp) (the latter next to the attention output in the
+// [L][H + F] buffer g), attention into g's first H columns, one GEMM over
+// K = H + F with the gated residual (biases b_o + b_2).
+acid_status block_forward_parallel(acid_model* m, int b, const float* mod6, float* h,
+                                   hipStream_t s, const int32_t* pred) {
+  const acid_dit_config& c = m->cfg;
+  const int H = c.hidden, F = c.ffn;
+  const int64_t L = m->L();
+  const int dt = c.dtype;
+  void* act = m->kp<void>(m->kl.act);
+  char* g = m->kp<char>(m->kl.g);
+  ACID_TRY(ln_mod(m, h, L, mod6, mod6 + H, act, s, pred));
+  acid_epilogue_args e = {};
+  e.kind = ACID_EPI_QKV_GELU;
+  e.bias = m->bp(b, m->wl.qkv_b);  // [b_qkv | b_1]
+  e.q = m->kp<void>(m->kl.q);
+  e.k = m->kp<void>(m->kl.k);
+  e.vt = m->kp<void>(m->kl.vt);
+  e.vt_ld = m->kl.vt_ld;
+  e.n_heads = c.n_heads;
+  e.head_dim = c.head_dim;
+  e.out = g + (size_t)H * esize(dt);
+  e.out_ld = H + F;
+  ACID_TRY(run(m, ACID_K_GEMM_QKV, s, "qkv+mlp gemm", [&]() {
+    return launch_linear(dt, L, 3 * H + F, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred);
+  }));
+  ACID_TRY(run(m, ACID_K_ATTENTION, s, "attention", [&]() {
+    return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, g, s, pred,
+                            H + F);
+  }));
+  acid_epilogue_args p = {};
+  p.kind = ACID_EPI_GATE_RESIDUAL;
+  p.bias = m->bp(b, m->wl.o_b);
+  p.bias2 = m->bp(b, m->wl.f2_b);
+  p.gate = mod6 + 2 * H;
+  p.out = h;
+  return run(m, ACID_K_GEMM_PROJ, s, "attn+mlp projection gemm", [&]() {
+    return launch_linear(dt, L, H, H + F, g, m->bp<void>(b, m->wl.o_w), p, s, pred);
+  });
 }
 
 // h = [text; x], all blocks with the modulation row `row`.
@@ -676,7 +730,8 @@ struct TensorInfo {
   int rank;
   int64_t d0, d1;
   int gemm;
-  size_t off;  // absolute offset in the arena
+  size_t off;   // absolute offset in the arena
+  int64_t ldd;  // GEMM operand row stride in elements (0: dense)
 };
 
 acid_status tensor_info(const acid_dit_config& c, int id, TensorInfo* t) {
@@ -684,10 +739,12 @@ acid_status tensor_info(const acid_dit_config& c, int id, TensorInfo* t) {
   const int nb = c.n_blocks;
   const WeightLayout L = weight_layout(c);
   if (id < 0 || id >= 8 + 10 * nb) return set_error(ACID_ERR_INVALID_ARG, "tensor id %d out of range", id);
-  auto set = [&](int rank, int64_t d0, int64_t d1, int gemm, size_t off) {
-    *t = TensorInfo{rank, d0, d1, gemm, off};
+  auto set = [&](int rank, int64_t d0, int64_t d1, int gemm, size_t off, int64_t ldd = 0) {
+    *t = TensorInfo{rank, d0, d1, gemm, off, ldd};
     return ACID_OK;
   };
+  const bool par = c.block_kind == ACID_BLOCK_PARALLEL;
+  const size_t es = esize(c.dtype);
   if (id < 4) {
     switch (id) {
       case 0: return set(2, Ft, H, 0, L.temb_w1);
@@ -704,11 +761,12 @@ acid_status tensor_info(const acid_dit_config& c, int id, TensorInfo* t) {
       case 1: return set(1, 6 * H, 1, 0, base + L.ada_b);
       case 2: return set(2, H, 3 * H, 1, base + L.qkv_w);
       case 3: return set(1, 3 * H, 1, 0, base + L.qkv_b);
-      case 4: return set(2, H, H, 1, base + L.o_w);
+      case 4: return par ? set(2, H, H, 1, base + L.o_w, H + F) : set(2, H, H, 1, base + L.o_w);
       case 5: return set(1, H, 1, 0, base + L.o_b);
       case 6: return set(2, H, F, 1, base + L.f1_w);
       case 7: return set(1, F, 1, 0, base + L.f1_b);
-      case 8: return set(2, F, H, 1, base + L.f2_w);
+      case 8:  // parallel: columns H .. H + F of the [H][H + F] operand
+        return par ? set(2, F, H, 1, base + L.o_w + H * es, H + F) : set(2, F, H, 1, base + L.f2_w);
       default: return set(1, H, 1, 0, base + L.f2_b);
     }
   }
@@ -749,6 +807,15 @@ acid_status acid_model_create(const acid_dit_config* cfg, void* weights_dev, voi
   m->ws = static_cast<char*>(workspace_dev);
   m->wl = weight_layout(*cfg);
   m->kl = work_layout(*cfg, max_steps);
+  {
+    const size_t H = cfg->hidden, es = esize(cfg->dtype);
+    const WeightLayout& w = m->wl;
+    if (w.f1_w != w.qkv_w + 3 * H * H * es || w.f1_b != w.qkv_b + 3 * H * 4 ||
+        w.f2_w != w.o_w + H * H * es) {
+      delete m;
+      return set_error(ACID_ERR_SHAPE, "weight layout: concatenated operands are not adjacent");
+    }
+  }
   *out = m;
   return ACID_OK;
 }
@@ -764,7 +831,8 @@ acid_status acid_model_load_tensor(acid_model* m, int32_t id, const float* src_d
                      (long long)n);
   void* dst = m->wb + t.off;
   return run(m, ACID_K_MISC, stream, "load tensor", [&]() {
-    if (t.gemm) return launch_transpose_convert(src_dev, t.d0, t.d1, m->cfg.dtype, dst, stream);
+    if (t.gemm)
+      return launch_transpose_convert(src_dev, t.d0, t.d1, m->cfg.dtype, dst, stream, t.ldd);
     return hipMemcpyAsync(dst, src_dev, (size_t)count * 4, hipMemcpyDeviceToDevice, stream);
   });
 }
@@ -871,6 +939,17 @@ acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K, const vo
         return set_error(ACID_ERR_SHAPE, "QKV: N must be 3 * n_heads * head_dim, head_dim % 32 == 0");
       if (epi->vt_ld < M) return set_error(ACID_ERR_SHAPE, "QKV: vt_ld < M");
       break;
+    case ACID_EPI_QKV_GELU: {
+      if (!epi->q || !epi->k || !epi->vt || !epi->out)
+        return set_error(ACID_ERR_INVALID_ARG, "q/k/vt/out NULL");
+      const int64_t nq = (int64_t)3 * epi->n_heads * epi->head_dim;
+      if (epi->head_dim < 1 || epi->n_heads < 1 || epi->head_dim % 32 || nq >= N || nq % 32)
+        return set_error(ACID_ERR_SHAPE,
+                         "QKV_GELU: 3 * n_heads * head_dim must be < N, head_dim % 32 == 0");
+      if (epi->vt_ld < M) return set_error(ACID_ERR_SHAPE, "QKV_GELU: vt_ld < M");
+      if (epi->out_ld < N - nq) return set_error(ACID_ERR_SHAPE, "QKV_GELU: out_ld < N - 3 H");
+      break;
+    }
     default: return set_error(ACID_ERR_INVALID_ARG, "bad epilogue kind %d", epi->kind);
   }
   hipError_t e = launch_linear(dtype, M, N, K, a_dev, wt_dev, *epi, stream);
