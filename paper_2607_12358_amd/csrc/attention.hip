@@ -483,72 +483,73 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
 
 // ------------------------------------------------------------------ fp32
 
-constexpr int FQ = 64, FKV = 32;
-
+// fp32 path (the small fp32 configuration): one wave per (head, query).
+// Lanes take one key each of a 64-key chunk for the scores; the wave max and
+// sum give the online softmax; lane l accumulates output dims l, l + 64, ...
+// over the chunk's probabilities, broadcast one key at a time.
 template <int D>
-__global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ Q,
-                                                      const float* __restrict__ Kp,
-                                                      const float* __restrict__ Vt, int64_t L,
-                                                      int64_t vt_ld, int n_heads,
-                                                      float* __restrict__ O, int64_t o_ld,
-                                                      float scale, const int32_t* pred) {
+__global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__ Q,
+                                                       const float* __restrict__ Kp,
+                                                       const float* __restrict__ Vt, int64_t L,
+                                                       int64_t vt_ld, int n_heads,
+                                                       float* __restrict__ O, int64_t o_ld,
+                                                       float scale, const int32_t* pred) {
   if (pred && *pred == 0) return;
-  __shared__ float Ks[FKV][D];
-  __shared__ float Vs[FKV][D + 1];
-  const int head = blockIdx.y;
-  const int t = threadIdx.x;
-  const int64_t qrow = (int64_t)blockIdx.x * FQ + t;
-  const float* Qh = Q + (int64_t)head * L * D;
+  constexpr int C = D / 64;  // output dims per lane
+  const int lane = threadIdx.x & 63;
+  const int64_t wq = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (wq >= L * n_heads) return;  // whole wave; no barriers below
+  const int head = (int)(wq / L);
+  const int64_t qrow = wq - (int64_t)head * L;
   const float* Kh = Kp + (int64_t)head * L * D;
   const float* Vh = Vt + (int64_t)head * D * vt_ld;
-  float q[D], o[D];
+  float q[D];
+  {
+    const float4* q4 = reinterpret_cast<const float4*>(Q + ((int64_t)head * L + qrow) * D);
 #pragma unroll
-  for (int d = 0; d < D; ++d) {
-    q[d] = qrow < L ? Qh[qrow * D + d] : 0.f;
-    o[d] = 0.f;
+    for (int d4 = 0; d4 < D / 4; ++d4) {
+      const float4 v = q4[d4];
+      q[4 * d4] = v.x;
+      q[4 * d4 + 1] = v.y;
+      q[4 * d4 + 2] = v.z;
+      q[4 * d4 + 3] = v.w;
+    }
   }
-  float m_run = -__builtin_inff(), l_run = 0.f;
-  for (int64_t j0 = 0; j0 < L; j0 += FKV) {
-    __syncthreads();
-    for (int idx = t; idx < FKV * D; idx += 64) {
-      const int j = idx / D, d = idx % D;
-      Ks[j][d] = (j0 + j < L) ? Kh[(j0 + j) * D + d] : 0.f;
-    }
-    for (int idx = t; idx < FKV * D; idx += 64) {
-      const int d = idx / FKV, j = idx % FKV;
-      Vs[j][d] = (j0 + j < L) ? Vh[(int64_t)d * vt_ld + j0 + j] : 0.f;
-    }
-    __syncthreads();
-    float sc[FKV];
-    float mx = -__builtin_inff();
+  float o[C];
 #pragma unroll
-    for (int j = 0; j < FKV; ++j) {
+  for (int c = 0; c < C; ++c) o[c] = 0.f;
+  float m_run = -__builtin_inff(), l_run = 0.f;
+  for (int64_t j0 = 0; j0 < L; j0 += 64) {
+    const int64_t j = j0 + lane;
+    float s = -__builtin_inff();
+    if (j < L) {
+      const float4* k4 = reinterpret_cast<const float4*>(Kh + j * D);
       float a = 0.f;
 #pragma unroll
-      for (int d = 0; d < D; ++d) a += q[d] * Ks[j][d];
-      sc[j] = (j0 + j < L) ? a * scale : -__builtin_inff();
-      mx = fmaxf(mx, sc[j]);
+      for (int d4 = 0; d4 < D / 4; ++d4) {
+        const float4 kv = k4[d4];
+        a += q[4 * d4] * kv.x + q[4 * d4 + 1] * kv.y + q[4 * d4 + 2] * kv.z + q[4 * d4 + 3] * kv.w;
+      }
+      s = a * scale;
     }
-    const float m_new = fmaxf(m_run, mx);
+    const float m_new = fmaxf(m_run, wave_max(s));  // finite: the chunk has a key
     const float alpha = expf(m_run - m_new);
     m_run = m_new;
-    l_run *= alpha;
+    const float p = j < L ? expf(s - m_new) : 0.f;
+    l_run = l_run * alpha + wave_sum(p);
 #pragma unroll
-    for (int d = 0; d < D; ++d) o[d] *= alpha;
+    for (int c = 0; c < C; ++c) o[c] *= alpha;
+    const int cnt = (int)(L - j0 < 64 ? L - j0 : 64);
+    for (int jj = 0; jj < cnt; ++jj) {
+      const float pj = __shfl(p, jj, 64);
 #pragma unroll
-    for (int j = 0; j < FKV; ++j) {
-      const float p = expf(sc[j] - m_new);
-      l_run += p;
-#pragma unroll
-      for (int d = 0; d < D; ++d) o[d] += p * Vs[j][d];
+      for (int c = 0; c < C; ++c) o[c] += pj * Vh[(int64_t)(lane + 64 * c) * vt_ld + j0 + jj];
     }
   }
-  if (qrow < L) {
-    const float inv = 1.0f / l_run;
-    float* orow = O + qrow * o_ld + (int64_t)head * D;
+  const float inv = 1.0f / l_run;
+  float* orow = O + qrow * o_ld + (int64_t)head * D;
 #pragma unroll
-    for (int d = 0; d < D; ++d) orow[d] = o[d] * inv;
-  }
+  for (int c = 0; c < C; ++c) orow[lane + 64 * c] = o[c] * inv;
 }
 
 // Waves per workgroup: 8 for d = 128 (a staged K/V tile feeds 256 queries),
@@ -578,8 +579,8 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
 template <int D>
 hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
                       int64_t vt_ld, void* o, int64_t o_ld, hipStream_t s, const int32_t* pred) {
-  dim3 grid((unsigned)((L + FQ - 1) / FQ), (unsigned)n_heads);
-  hipLaunchKernelGGL(attn_f32_kernel<D>, grid, dim3(64), 0, s, (const float*)q,
+  dim3 grid((unsigned)((L * n_heads + 3) / 4));
+  hipLaunchKernelGGL(attn_f32_kernel<D>, grid, dim3(256), 0, s, (const float*)q,
                      (const float*)k, (const float*)vt, L, vt_ld, n_heads, (float*)o, o_ld,
                      1.0f / sqrtf((float)D), pred);
   return hipGetLastError();
