@@ -209,6 +209,17 @@ def test_linear(P, kind, dtype, M, N, K):
         assert e < tol, (kind, e)
 
 
+@pytest.mark.parametrize("kind", KINDS)
+def test_linear_large_tiles_ragged(P, kind):
+    """Large ragged shapes: ragged M over many 256-row tiles and, for
+    N = 2176, a half-width last feature tile."""
+    M, K = 8200, 256
+    N = 2304 if kind == "qkv" else 2176
+    # the qkv case in _linear_case uses d = 64: 2304 = 3 x 12 x 64
+    for got, ref, tol in _linear_case(P, kind, M, N, K, torch.bfloat16, seed=17):
+        assert rel_err(got, ref) < tol, kind
+
+
 def test_linear_shape_errors(P):
     a = torch.zeros((4, 128), dtype=torch.bfloat16, device="cuda")
     wt = torch.zeros((100, 128), dtype=torch.bfloat16, device="cuda")
