@@ -257,8 +257,8 @@ def main() -> int:
                     help="host: gate on the host, one drift read-back per step; graph: gate on "
                          "the device, the loop captured once as a HIP graph and replayed "
                          "(teacache signal)")
-    ap.add_argument("--no-graph-context", action="store_true",
-                    help="skip timing the other loop variant as context")
+    ap.add_argument("--graph-context", action="store_true",
+                    help="also time the other loop variant (host gate / captured graph)")
     ap.add_argument("--no-nocache", action="store_true", help="skip the uncached context loop")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="disable the per-kernel event timer")
@@ -390,7 +390,7 @@ def main() -> int:
     log(f"{args.steps} loops ({args.loop}) -> {s_per_loop:.4f} s/loop, {n_comp}/{N} computed")
 
     other = None
-    if mode == "acid" and not args.no_graph_context:
+    if mode == "acid" and args.graph_context:
         x.copy_(x0)
         m.denoise_loop(x, sig, text_d, mode=mode, **gate, graph=not graph)  # warm / capture
         other, _, _ = loops(args.steps, not graph, False, "context")
