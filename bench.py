@@ -219,10 +219,7 @@ def run_sweep(args, m, cfg, x0, text_d, sig, mode: str = "acid") -> int:
         sv = [float(v) for v in tr["s"] if math.isfinite(v)]
         ds = [abs(a - b) for a, b in zip(sv[1:], sv[:-1])]
         run = {"mode": kind, "tau_low": lo, "tau_high": hi, "delta": delta,
-               "loop": args.loop,
-        "host_loop_s_per_loop": other if graph else s_per_loop,
-        "graph_loop_s_per_loop": s_per_loop if graph else other,
-        "computed_steps": n_comp, "s_per_loop": t, "speedup_vs_nocache": t_ref / t,
+               "computed_steps": n_comp, "s_per_loop": t, "speedup_vs_nocache": t_ref / t,
                "psnr_db": psnr(x, ref),
                "steps_tau_high": int(sum(1 for v in tr["tau_used"][1:] if v == hi)),
                "drift_s_min_max": [min(sv), max(sv)] if sv else None,
