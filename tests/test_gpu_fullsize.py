@@ -3,8 +3,8 @@ benchmark times, on outputs the oracle can compute one by one (sampled query
 rows / token rows), plus properties that hold at any size.
 
 Shapes: Wan-2.1-1.3B (12 x 32760 x 128, H 1536, F 8960), CogVideoX-5B
-(48 x 17776 x 64, H 3072, F 12288) and the HunyuanVideo slice
-(24 x 119056 x 128).  Inputs are seeded torch / NumPy draws; bf16 operands
+(48 x 17776 x 64, H 3072, F 12288; one block in both the sequential and the
+parallel form) and the HunyuanVideo slice (24 x 119056 x 128).  Inputs are seeded torch / NumPy draws; bf16 operands
 are compared with an oracle fed the same bf16 values.
 """
 import math
@@ -131,6 +131,30 @@ def test_block_fullsize_wan_sampled(P, wan_block):
     ref = om.block(h0, 0, mod6.astype(np.float64), rows=rows)
     got = to_np(h[rows])
     assert rel_err(got - h0[rows], ref - h0[rows]) < 2e-2
+    assert np.all(np.isfinite(to_np(h)))
+
+
+@pytest.mark.parametrize("block", ["sequential", "parallel"])
+def test_block_fullsize_cogvideox_sampled(P, block):
+    """One block at the CogVideoX-5B shape (226 text + 17550 video tokens,
+    48 x 64 heads, H 3072, F 12288, bf16) in both block forms, on sampled
+    rows (text rows, video rows, both ends) against the oracle's block with
+    K/V over all tokens."""
+    cfg = ai.COG5B.replace(n_blocks=1, n_steps=2, block=block)
+    m, params = make_model(P, cfg, max_steps=2)
+    om = O.DiTModel(cfg, params)
+    H = cfg.hidden
+    h0 = ai.gaussian((cfg.n_tokens, H), 23)
+    mod6 = om.modulation(0.41)["blocks"][0].astype(np.float32)
+    h = to_dev(h0)
+    m.block_forward(0, to_dev(mod6), h)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(6)
+    rows = np.unique(np.concatenate([rng.choice(cfg.n_text, 8, replace=False),
+                                     cfg.n_text + rng.choice(cfg.n_video, 32, replace=False),
+                                     [0, cfg.n_text - 1, cfg.n_text, cfg.n_tokens - 1]]))
+    ref = om.block(h0, 0, mod6.astype(np.float64), rows=rows)
+    assert rel_err(to_np(h[rows]) - h0[rows], ref - h0[rows]) < 2e-2
     assert np.all(np.isfinite(to_np(h)))
 
 
