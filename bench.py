@@ -251,9 +251,8 @@ def main() -> int:
                     help="default 0.2 (both signals)")
     ap.add_argument("--delta", type=float, default=0.01)
     ap.add_argument("--loop", choices=["host", "graph"], default="host",
-                    help="host: gate on the host, one drift read-back per step; graph: gate on "
-                         "the device, the loop captured once as a HIP graph and replayed "
-                         "(teacache signal)")
+                    help="host: gate on the host, one signal read-back per step; graph: gate "
+                         "on the device, the loop captured once as a HIP graph and replayed")
     ap.add_argument("--graph-context", action="store_true",
                     help="also time the other loop variant (host gate / captured graph)")
     ap.add_argument("--no-nocache", action="store_true", help="skip the uncached context loop")
@@ -336,9 +335,6 @@ def main() -> int:
 
     if args.sweep:
         return run_sweep(args, m, cfg, x0, text_d, sig, mode)
-    if args.loop == "graph" and mode != "acid":
-        print("--loop graph runs the teacache signal (the device gate's input)", file=sys.stderr)
-        return 2
     graph = args.loop == "graph"
 
     def loops(count, use_graph, timed_kernels, label):
@@ -387,7 +383,7 @@ def main() -> int:
     log(f"{args.steps} loops ({args.loop}) -> {s_per_loop:.4f} s/loop, {n_comp}/{N} computed")
 
     other = None
-    if mode == "acid" and args.graph_context:
+    if args.graph_context:
         x.copy_(x0)
         m.denoise_loop(x, sig, text_d, mode=mode, **gate, graph=not graph)  # warm / capture
         other, _, _ = loops(args.steps, not graph, False, "context")

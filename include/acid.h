@@ -295,13 +295,14 @@ acid_status acid_denoise_loop(acid_model* m, float* x_dev,
 
 /* The same loop with the gate on the device and no host round trip between
  * steps (Section 3.3's gate and the loop of Algorithm 1; the gate's low cost
- * is the paper's claim, Section 3.2).  NOCACHE and ACID modes only
- * (ACID_ERR_UNSUPPORTED otherwise); arguments, results and trace as
- * acid_denoise_loop, to the bit.  Per ACID step a one-thread kernel runs the
- * gate step on the drift the reduction left in device memory and writes the
- * decision into a device trace; every model kernel of the step reads that
- * word and exits at once when it is 0, and the cache kernel takes STORE or
- * APPLY from it.  The modulation table is computed on `stream` first; the
+ * is the paper's claim, Section 3.2).  Every mode; arguments, results and
+ * trace as acid_denoise_loop, to the bit.  Per step a one-thread kernel runs
+ * the gate step on the signal the reductions left in device memory (the
+ * TEMNI drift, DiCache's probe change, or EasyCache's k |dx| / |v_prev|,
+ * with k kept on the device) and writes the decision into a device trace
+ * and its negation into a skip word; every kernel that runs only on a
+ * computed (or only on a skipped) step reads that word and exits at once
+ * when it says so, and the cache kernel takes STORE or APPLY from it.  The modulation table is computed on `stream` first; the
  * per-step launches are captured once into a HIP graph (on a stream the
  * model owns) and replayed on `stream` by later calls with the same x_dev,
  * text_dev, n_steps, sigmas, mode, gate and forced schedule; any change
@@ -315,6 +316,8 @@ acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev,
                                     const uint8_t* forced_schedule_host,
                                     acid_step_trace* trace_host,
                                     hipStream_t stream);
+/* (The DiCache probe depth, acid_model_set_probe_blocks, is part of what a
+ * captured graph is keyed on.) */
 
 /* Algorithm 1 (Section 3.3) on the device, one thread, over n signals
  * s_dev[0..n) (fp64, device; NaN where a step has no signal) from the

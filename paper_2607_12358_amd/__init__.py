@@ -248,8 +248,8 @@ class Model:
         "nocache", "acid" (TeaCache's signal), "easycache" or "dicache"
         (probe depth: set_probe_blocks); n_warmup defaults to 1 (2 for
         "easycache").  graph=True runs the device-gate loop captured as a
-        HIP graph ("nocache" and "acid"); with trace=False it returns None
-        without waiting for the GPU."""
+        HIP graph (any mode); with trace=False it returns None without
+        waiting for the GPU."""
         sig = np.ascontiguousarray(sigmas, dtype=np.float32)
         n = len(sig) - 1
         modes = {"acid": ACID_MODE_ACID, "nocache": ACID_MODE_NOCACHE,

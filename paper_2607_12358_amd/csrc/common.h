@@ -80,24 +80,32 @@ hipError_t launch_temni_drift(const float* x, int64_t rows, int H, const float* 
 // Fixed-order reduction of per-row (num, den) pairs -> out[0]=num, out[1]=den, out[2]=s.
 hipError_t launch_drift_finalize(const double* partials, int64_t rows, double* out,
                                  hipStream_t s);
-// With `flag` (a device int32) the operation is STORE if *flag, else APPLY.
+// With `flag` (a device int32) the operation is STORE if *flag, else APPLY;
+// without it, op, skipped when predicated off.
 hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n,
-                        hipStream_t s, const int32_t* flag = nullptr);
+                        hipStream_t s, const int32_t* flag = nullptr,
+                        const int32_t* pred = nullptr);
 // dst = src (n floats, 16-byte aligned) unless predicated off.
 hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s,
                        const int32_t* pred);
-// One step of Algorithm 1 on the device; see gate_step_kernel.
-hipError_t launch_gate_step(const double* res, int has_signal, const acid_gate_params& p,
-                            int forced, int step_index, acid_gate_state* st,
-                            acid_step_trace* tr, hipStream_t s);
+// One step of Algorithm 1 on the device; see gate_step_kernel.  sig_kind is
+// an acid_mode (ACID: TeaCache's drift).
+hipError_t launch_gate_step(const double* res, int sig_kind, int has_signal,
+                            const acid_gate_params& p, int forced, int step_index,
+                            acid_gate_state* st, acid_step_trace* tr, int32_t* skip, double* ec,
+                            hipStream_t s);
+// EasyCache's rate update on the device; see easycache_rate_kernel.
+hipError_t launch_easycache_rate(const double* res, double* ec, const int32_t* pred,
+                                 hipStream_t s);
 // Algorithm 1 over a signal sequence on the device.
 hipError_t launch_gate_sequence(const double* sig, int n, const acid_gate_params& p,
                                 acid_step_trace* tr, hipStream_t s);
 // fp32 [in][out] -> [out][in] in dtype
 hipError_t launch_l1_norms(const float* a, const float* b, const float* c, int64_t n,
-                           double* partials, int max_groups, double* out, hipStream_t s);
+                           double* partials, int max_groups, double* out, hipStream_t s,
+                           const int32_t* pred = nullptr);
 hipError_t launch_easycache_reuse(float* x, float* xp, float* v, const float* d, int64_t n,
-                                  float dsig, hipStream_t s);
+                                  float dsig, hipStream_t s, const int32_t* pred = nullptr);
 // dst row o at dst + o * ldd (ldd 0: in).
 hipError_t launch_transpose_convert(const float* src, int64_t in, int64_t out, int dtype,
                                     void* dst, hipStream_t s, int64_t ldd = 0);

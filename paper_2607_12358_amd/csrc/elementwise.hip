@@ -201,7 +201,9 @@ __device__ __forceinline__ void cache_body(const float* __restrict__ x, float* _
 template <int OP>
 __global__ __launch_bounds__(256) void cache_kernel(const float* __restrict__ x,
                                                     float* __restrict__ h,
-                                                    float* __restrict__ r, int64_t n) {
+                                                    float* __restrict__ r, int64_t n,
+                                                    const int32_t* __restrict__ pred) {
+  if (pred && *pred == 0) return;
   cache_body<OP>(x, h, r, n);
 }
 
@@ -232,15 +234,25 @@ __global__ __launch_bounds__(256) void copy_pred_kernel(const float* __restrict_
   if (blockIdx.x == 0 && threadIdx.x < (n & 3)) dst[n4 * 4 + threadIdx.x] = src[n4 * 4 + threadIdx.x];
 }
 
+// num / den with 0 / 0 = 0 and num / 0 = +inf (the host loops' rule).
+__device__ __forceinline__ double ratio_or_inf_dev(double num, double den) {
+  if (den == 0.0) return num == 0.0 ? 0.0 : __builtin_inf();
+  return num / den;
+}
+
 // Device-resident gate, one step of Algorithm 1 per launch (one thread).
-// The signal is res[2] (the drift reduction's output) when has_signal, else
-// NaN.  step_index 0 starts from the initial state.  The decision goes to
+// The signal, when has_signal (else NaN), by kind: TeaCache res[2] (the
+// drift reduction's output); DiCache res[0] / res[1] (the probe's relative
+// L1 change); EasyCache k res[0] / res[1] once a rate k exists (ec[0], with
+// ec[1] != 0), and res[0] = |x_i - x_{i-1}| is kept in ec[2] for the rate
+// update.  step_index 0 starts from the initial state.  The decision goes to
 // tr->compute (the predicate of the step's model kernels): the gate's own,
-// or forced (0/1) when forced >= 0.
-__global__ void gate_step_kernel(const double* __restrict__ res, int has_signal,
+// or forced (0/1) when forced >= 0; *skip receives its negation.
+__global__ void gate_step_kernel(const double* __restrict__ res, int sig_kind, int has_signal,
                                  acid_gate_params p, int forced, int step_index,
                                  acid_gate_state* __restrict__ st,
-                                 acid_step_trace* __restrict__ tr) {
+                                 acid_step_trace* __restrict__ tr, int32_t* __restrict__ skip,
+                                 double* __restrict__ ec) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   acid_gate_state g;
   if (step_index == 0) {
@@ -248,15 +260,31 @@ __global__ void gate_step_kernel(const double* __restrict__ res, int has_signal,
     g.s_prev = 0.0;
     g.has_prev = 0;
     g.step = 0;
+    if (ec) {
+      ec[0] = __builtin_nan("");
+      ec[1] = 0.0;
+      ec[2] = __builtin_nan("");
+    }
   } else {
     g = *st;
   }
-  const double s = has_signal ? res[2] : __builtin_nan("");
+  double s = __builtin_nan("");
+  if (has_signal) {
+    if (sig_kind == ACID_MODE_DICACHE) {
+      s = ratio_or_inf_dev(res[0], res[1]);
+    } else if (sig_kind == ACID_MODE_EASYCACHE) {
+      if (ec[1] != 0.0) s = ec[0] * ratio_or_inf_dev(res[0], res[1]);
+      ec[2] = res[0];
+    } else {
+      s = res[2];
+    }
+  }
   double tau;
   const int32_t c = gate_step(&g, &p, s, &tau);
   *st = g;
   acid_step_trace t;
   t.compute = forced >= 0 ? forced : c;
+  *skip = !t.compute;
   t.gate_compute = c;
   t.s = s;
   t.sigma_sum_after = g.sigma_sum;
@@ -308,7 +336,9 @@ template <bool HAS_B, bool HAS_C>
 __global__ __launch_bounds__(256) void l1_partials_kernel(const float* __restrict__ a,
                                                           const float* __restrict__ b,
                                                           const float* __restrict__ c,
-                                                          int64_t n, double* __restrict__ part) {
+                                                          int64_t n, double* __restrict__ part,
+                                                          const int32_t* __restrict__ pred) {
+  if (pred && *pred == 0) return;  // whole block: pred is uniform
   __shared__ double lds[4];
   const int64_t n4 = n >> 2;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -343,7 +373,9 @@ __global__ __launch_bounds__(256) void l1_partials_kernel(const float* __restric
 
 // Fixed-order sum of G partial pairs: out[0], out[1].
 __global__ __launch_bounds__(1024) void l1_finalize_kernel(const double* __restrict__ part, int G,
-                                                           double* __restrict__ out) {
+                                                           double* __restrict__ out,
+                                                           const int32_t* __restrict__ pred) {
+  if (pred && *pred == 0) return;
   __shared__ double s0[1024], s1[1024];
   const int t = threadIdx.x;
   double u = 0.0, w = 0.0;
@@ -372,7 +404,9 @@ __global__ __launch_bounds__(256) void easycache_reuse_kernel(float* __restrict_
                                                               float* __restrict__ xp,
                                                               float* __restrict__ v,
                                                               const float* __restrict__ d,
-                                                              int64_t n, float dsig) {
+                                                              int64_t n, float dsig,
+                                                              const int32_t* __restrict__ pred) {
+  if (pred && *pred == 0) return;
   const int64_t n4 = n >> 2;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   float4* x4 = reinterpret_cast<float4*>(x);
@@ -484,15 +518,15 @@ static unsigned stream_grid(int64_t n) {
 }
 
 hipError_t launch_cache(int op, const float* x, float* h, float* r, int64_t n, hipStream_t s,
-                        const int32_t* flag) {
+                        const int32_t* flag, const int32_t* pred) {
   if (n == 0) return hipSuccess;
   const unsigned blocks = stream_grid(n);
   if (flag)
     hipLaunchKernelGGL(cache_by_flag_kernel, dim3(blocks), dim3(256), 0, s, x, h, r, n, flag);
   else if (op == ACID_CACHE_STORE)
-    hipLaunchKernelGGL(cache_kernel<ACID_CACHE_STORE>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
+    hipLaunchKernelGGL(cache_kernel<ACID_CACHE_STORE>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n, pred);
   else
-    hipLaunchKernelGGL(cache_kernel<ACID_CACHE_APPLY>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n);
+    hipLaunchKernelGGL(cache_kernel<ACID_CACHE_APPLY>, dim3((unsigned)blocks), dim3(256), 0, s, x, h, r, n, pred);
   return hipGetLastError();
 }
 
@@ -511,11 +545,28 @@ hipError_t launch_copy(const float* src, float* dst, int64_t n, hipStream_t s,
   return hipGetLastError();
 }
 
-hipError_t launch_gate_step(const double* res, int has_signal, const acid_gate_params& p,
-                            int forced, int step_index, acid_gate_state* st,
-                            acid_step_trace* tr, hipStream_t s) {
-  hipLaunchKernelGGL(gate_step_kernel, dim3(1), dim3(64), 0, s, res, has_signal, p, forced,
-                     step_index, st, tr);
+hipError_t launch_gate_step(const double* res, int sig_kind, int has_signal,
+                            const acid_gate_params& p, int forced, int step_index,
+                            acid_gate_state* st, acid_step_trace* tr, int32_t* skip, double* ec,
+                            hipStream_t s) {
+  hipLaunchKernelGGL(gate_step_kernel, dim3(1), dim3(64), 0, s, res, sig_kind, has_signal, p,
+                     forced, step_index, st, tr, skip, ec);
+  return hipGetLastError();
+}
+
+// EasyCache's rate after a computed step: k = |v_i - v_{i-1}| / |x_i - x_{i-1}|
+// (res[0] over the kept ec[2]), one thread, unless predicated off.
+__global__ void easycache_rate_kernel(const double* __restrict__ res, double* __restrict__ ec,
+                                      const int32_t* __restrict__ pred) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  if (pred && *pred == 0) return;
+  ec[0] = ratio_or_inf_dev(res[0], ec[2]);
+  ec[1] = 1.0;
+}
+
+hipError_t launch_easycache_rate(const double* res, double* ec, const int32_t* pred,
+                                 hipStream_t s) {
+  hipLaunchKernelGGL(easycache_rate_kernel, dim3(1), dim3(64), 0, s, res, ec, pred);
   return hipGetLastError();
 }
 
@@ -527,26 +578,27 @@ hipError_t launch_gate_sequence(const double* sig, int n, const acid_gate_params
 }
 
 hipError_t launch_l1_norms(const float* a, const float* b, const float* c, int64_t n,
-                           double* partials, int max_groups, double* out, hipStream_t s) {
+                           double* partials, int max_groups, double* out, hipStream_t s,
+                           const int32_t* pred) {
   const int G = l1_grid(n, max_groups);
 #define L1K(HB, HC) \
-  hipLaunchKernelGGL((l1_partials_kernel<HB, HC>), dim3(G), dim3(256), 0, s, a, b, c, n, partials)
+  hipLaunchKernelGGL((l1_partials_kernel<HB, HC>), dim3(G), dim3(256), 0, s, a, b, c, n, partials, pred)
   if (b && c) L1K(true, true);
   else if (b) L1K(true, false);
   else if (c) L1K(false, true);
   else L1K(false, false);
 #undef L1K
-  hipLaunchKernelGGL(l1_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, G, out);
+  hipLaunchKernelGGL(l1_finalize_kernel, dim3(1), dim3(1024), 0, s, partials, G, out, pred);
   return hipGetLastError();
 }
 
 hipError_t launch_easycache_reuse(float* x, float* xp, float* v, const float* d, int64_t n,
-                                  float dsig, hipStream_t s) {
+                                  float dsig, hipStream_t s, const int32_t* pred) {
   if (n == 0) return hipSuccess;
   int64_t blocks = ((n + 3) / 4 + 255) / 256;
   if (blocks > 256 * 16) blocks = 256 * 16;
   hipLaunchKernelGGL(easycache_reuse_kernel, dim3((unsigned)blocks), dim3(256), 0, s, x, xp, v, d,
-                     n, dsig);
+                     n, dsig, pred);
   return hipGetLastError();
 }
 

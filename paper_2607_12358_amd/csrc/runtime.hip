@@ -117,6 +117,7 @@ WeightLayout weight_layout(const acid_dit_config& c) {
 struct WorkLayout {
   size_t h, act, q, k, vt, o, g, modtab, temb_e, temb_hid, temb_u, partials, dres, m0, m1, r, v;
   size_t dtrace, gstate;  // device-resident gate: per-step trace, state
+  size_t dskip, ecst;     // per-step skip words; EasyCache (k, have k, |dx|)
   size_t total;
   int64_t vt_ld;
 };
@@ -153,6 +154,8 @@ WorkLayout work_layout(const acid_dit_config& c, int max_steps) {
   W.v = put(Lv * H * 4);
   W.dtrace = put(S * sizeof(acid_step_trace));
   W.gstate = put(sizeof(acid_gate_state));
+  W.dskip = put(S * sizeof(int32_t));
+  W.ecst = put(4 * sizeof(double));
   W.total = off;
   return W;
 }
@@ -188,12 +191,12 @@ struct acid_model {
   struct GraphKey {
     float* x = nullptr;
     const float* text = nullptr;
-    int n = 0, mode = -1;
+    int n = 0, mode = -1, probe = 0;
     acid_gate_params gate = {};
     std::vector<float> sigmas;
     std::vector<uint8_t> forced;
     bool operator==(const GraphKey& o) const {
-      return x == o.x && text == o.text && n == o.n && mode == o.mode &&
+      return x == o.x && text == o.text && n == o.n && mode == o.mode && probe == o.probe &&
              gate.tau_low == o.gate.tau_low && gate.tau_high == o.gate.tau_high &&
              gate.delta == o.gate.delta && gate.n_warmup == o.gate.n_warmup &&
              sigmas == o.sigmas && forced == o.forced;
@@ -444,12 +447,13 @@ acid_status stack_forward(acid_model* m, const float* row, const float* x, const
 
 // v = LN-modulated head of h_v; EULER variant updates x in place.
 acid_status head_forward(acid_model* m, const float* row, const float* hv, float* v_out,
-                         float* x_euler, float dsigma, hipStream_t s) {
+                         float* x_euler, float dsigma, hipStream_t s,
+                         const int32_t* pred = nullptr) {
   const acid_dit_config& c = m->cfg;
   const int H = c.hidden;
   const float* shift = row + 6 * (int64_t)c.n_blocks * H;
   void* act = m->kp<void>(m->kl.act);
-  ACID_TRY(ln_mod(m, hv, m->Lv(), shift, shift + H, act, s));
+  ACID_TRY(ln_mod(m, hv, m->Lv(), shift, shift + H, act, s, pred));
   acid_epilogue_args e = {};
   e.bias = m->wp(m->wl.head_b);
   if (x_euler) {
@@ -462,7 +466,7 @@ acid_status head_forward(acid_model* m, const float* row, const float* hv, float
     e.out = v_out;
   }
   return run(m, ACID_K_GEMM_HEAD, s, "head gemm", [&]() {
-    return launch_linear(c.dtype, m->Lv(), H, H, act, m->wp<void>(m->wl.head_w), e, s);
+    return launch_linear(c.dtype, m->Lv(), H, H, act, m->wp<void>(m->wl.head_w), e, s, pred);
   });
 }
 
@@ -673,7 +677,8 @@ acid_status enqueue_device_gate_loop(acid_model* m, float* x, const float* sig, 
       cur ^= 1;
       const int f = forced ? (forced[i] != 0) : -1;
       ACID_TRY(run(m, ACID_K_DRIFT, s, "device gate", [&]() {
-        return launch_gate_step(dres, i > 0, *gate, f, i, gst, dtr + i, s);
+        return launch_gate_step(dres, ACID_MODE_ACID, i > 0, *gate, f, i, gst, dtr + i,
+                                m->kp<int32_t>(m->kl.dskip) + i, nullptr, s);
       }));
       pred = &dtr[i].compute;
     }
@@ -685,6 +690,119 @@ acid_status enqueue_device_gate_loop(acid_model* m, float* x, const float* sig, 
       }));
     }
     ACID_TRY(head_forward(m, row, hv, nullptr, x, sig[i + 1] - sig[i], s));
+  }
+  return ACID_OK;
+}
+
+// DiCache's loop with the gate on the device: every step assembles the
+// residual stream, runs the probe blocks and keeps the probe's video rows;
+// the L1 sums against the previous probe stay in device memory for the gate;
+// the deep blocks are predicated on the decision, the cache kernel stores
+// or applies the deep residual, and the head runs every step.
+acid_status enqueue_dicache_graph_loop(acid_model* m, float* x, const float* sig, int n,
+                                       const float* text, const acid_gate_params* gate,
+                                       const uint8_t* forced, hipStream_t s) {
+  const int H = m->H();
+  const int64_t nv = m->Lv() * H;
+  const int np = m->probe_blocks;
+  const float* table = m->kp(m->kl.modtab);
+  float* pbuf[2] = {m->kp(m->kl.m0), m->kp(m->kl.m1)};
+  float* rdeep = m->kp(m->kl.r);
+  float* hv = m->kp(m->kl.h) + m->Lt() * H;
+  double* part = m->kp<double>(m->kl.partials);
+  double* dres = m->kp<double>(m->kl.dres);
+  const int max_groups = (int)(m->Lv() < 1024 ? m->Lv() : 1024);
+  acid_step_trace* dtr = m->kp<acid_step_trace>(m->kl.dtrace);
+  acid_gate_state* gst = m->kp<acid_gate_state>(m->kl.gstate);
+  int32_t* dskip = m->kp<int32_t>(m->kl.dskip);
+  int cur = 0;
+  for (int i = 0; i < n; ++i) {
+    const float* row = table + (int64_t)i * m->rowsz();
+    ACID_TRY(stack_assemble_pred(m, x, text, nullptr, s));
+    ACID_TRY(stack_blocks(m, row, 0, np, s));
+    float* p = pbuf[cur];
+    ACID_TRY(run(m, ACID_K_MISC, s, "keep probe features", [&]() {
+      return launch_copy(hv, p, nv, s, nullptr);
+    }));
+    if (i > 0) {
+      ACID_TRY(run(m, ACID_K_DRIFT, s, "probe l1 norms", [&]() {
+        return launch_l1_norms(p, pbuf[cur ^ 1], pbuf[cur ^ 1], nv, part, max_groups, dres, s);
+      }));
+    }
+    const int f = forced ? (forced[i] != 0) : -1;
+    ACID_TRY(run(m, ACID_K_DRIFT, s, "device gate", [&]() {
+      return launch_gate_step(dres, ACID_MODE_DICACHE, i > 0, *gate, f, i, gst, dtr + i,
+                              dskip + i, nullptr, s);
+    }));
+    const int32_t* pred = &dtr[i].compute;
+    ACID_TRY(stack_blocks(m, row, np, m->cfg.n_blocks, s, pred));
+    ACID_TRY(run(m, ACID_K_CACHE, s, "deep residual store/apply", [&]() {
+      return launch_cache(ACID_CACHE_STORE, p, hv, rdeep, nv, s, pred);
+    }));
+    ACID_TRY(head_forward(m, row, hv, nullptr, x, sig[i + 1] - sig[i], s));
+    cur ^= 1;
+  }
+  return ACID_OK;
+}
+
+// EasyCache's loop with the gate on the device: per step the L1 sums of
+// x_i - x_{i-1} and v_{i-1} feed the gate; a computed step (predicated on the
+// decision) keeps x_i, runs the stack and the head (v_i, Euler update),
+// stores D = v_i - x_i and updates the rate k from |v_i - v_{i-1}|; a skipped
+// step (predicated on its negation) reuses v = x + D.
+acid_status enqueue_easycache_graph_loop(acid_model* m, float* x, const float* sig, int n,
+                                         const float* text, const acid_gate_params* gate,
+                                         const uint8_t* forced, hipStream_t s) {
+  const int H = m->H();
+  const int64_t nv = m->Lv() * H;
+  const float* table = m->kp(m->kl.modtab);
+  float* xprev = m->kp(m->kl.m0);
+  float* vbuf[2] = {m->kp(m->kl.v), m->kp(m->kl.m1)};
+  float* offset = m->kp(m->kl.r);
+  float* hv = m->kp(m->kl.h) + m->Lt() * H;
+  double* part = m->kp<double>(m->kl.partials);
+  double* dres = m->kp<double>(m->kl.dres);
+  const int max_groups = (int)(m->Lv() < 1024 ? m->Lv() : 1024);
+  acid_step_trace* dtr = m->kp<acid_step_trace>(m->kl.dtrace);
+  acid_gate_state* gst = m->kp<acid_gate_state>(m->kl.gstate);
+  int32_t* dskip = m->kp<int32_t>(m->kl.dskip);
+  double* ec = m->kp<double>(m->kl.ecst);
+  int cur = 0;
+  for (int i = 0; i < n; ++i) {
+    const float* row = table + (int64_t)i * m->rowsz();
+    if (i > 0) {
+      ACID_TRY(run(m, ACID_K_DRIFT, s, "l1 norms", [&]() {
+        return launch_l1_norms(x, xprev, vbuf[cur ^ 1], nv, part, max_groups, dres, s);
+      }));
+    }
+    const int f = forced ? (forced[i] != 0) : -1;
+    ACID_TRY(run(m, ACID_K_DRIFT, s, "device gate", [&]() {
+      return launch_gate_step(dres, ACID_MODE_EASYCACHE, i > 0, *gate, f, i, gst, dtr + i,
+                              dskip + i, ec, s);
+    }));
+    const int32_t* pred = &dtr[i].compute;
+    const int32_t* spred = dskip + i;
+    const float dsig = sig[i + 1] - sig[i];
+    float* v = vbuf[cur];
+    ACID_TRY(run(m, ACID_K_MISC, s, "keep x_i", [&]() { return launch_copy(x, xprev, nv, s, pred); }));
+    ACID_TRY(stack_assemble_pred(m, x, text, pred, s));
+    ACID_TRY(stack_blocks(m, row, 0, m->cfg.n_blocks, s, pred));
+    ACID_TRY(head_forward(m, row, hv, v, x, dsig, s, pred));  // v_i; x <- x_{i+1}
+    ACID_TRY(run(m, ACID_K_CACHE, s, "offset store", [&]() {
+      return launch_cache(ACID_CACHE_STORE, xprev, v, offset, nv, s, nullptr, pred);  // D = v_i - x_i
+    }));
+    if (i > 0) {
+      ACID_TRY(run(m, ACID_K_DRIFT, s, "rate l1 norms", [&]() {
+        hipError_t e = launch_l1_norms(v, vbuf[cur ^ 1], nullptr, nv, part, max_groups, dres, s,
+                                       pred);
+        if (e == hipSuccess) e = launch_easycache_rate(dres, ec, pred, s);
+        return e;
+      }));
+    }
+    ACID_TRY(run(m, ACID_K_CACHE, s, "easycache reuse", [&]() {
+      return launch_easycache_reuse(x, xprev, v, offset, nv, dsig, s, spred);
+    }));
+    cur ^= 1;
   }
   return ACID_OK;
 }
@@ -1108,9 +1226,6 @@ acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev, const float* si
                                     const acid_gate_params* gate, const uint8_t* forced,
                                     acid_step_trace* trace, hipStream_t stream) {
   ACID_TRY(check_loop_args(m, x_dev, sigmas_host, n_steps, text_dev, mode, gate, forced));
-  if (mode != ACID_MODE_NOCACHE && mode != ACID_MODE_ACID)
-    return set_error(ACID_ERR_UNSUPPORTED,
-                     "the captured loop supports the NOCACHE and ACID modes (got %d)", mode);
   ACID_TRY(modulation_table(m, sigmas_host, n_steps, m->kp(m->kl.modtab), stream));
 
   acid_model::GraphKey key;
@@ -1118,6 +1233,7 @@ acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev, const float* si
   key.text = text_dev;
   key.n = n_steps;
   key.mode = mode;
+  key.probe = mode == ACID_MODE_DICACHE ? m->probe_blocks : 0;
   if (gate) key.gate = *gate;
   key.sigmas.assign(sigmas_host, sigmas_host + n_steps + 1);
   if (forced) key.forced.assign(forced, forced + n_steps);
@@ -1129,8 +1245,16 @@ acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev, const float* si
     if (!m->cap) ACID_HIP(hipStreamCreateWithFlags(&m->cap, hipStreamNonBlocking));
     ACID_HIP(hipStreamBeginCapture(m->cap, hipStreamCaptureModeRelaxed));
     m->capturing = true;
-    const acid_status st = enqueue_device_gate_loop(m, x_dev, sigmas_host, n_steps, text_dev,
-                                                    mode, gate, forced, m->cap);
+    acid_status st;
+    if (mode == ACID_MODE_DICACHE)
+      st = enqueue_dicache_graph_loop(m, x_dev, sigmas_host, n_steps, text_dev, gate, forced,
+                                      m->cap);
+    else if (mode == ACID_MODE_EASYCACHE)
+      st = enqueue_easycache_graph_loop(m, x_dev, sigmas_host, n_steps, text_dev, gate, forced,
+                                        m->cap);
+    else
+      st = enqueue_device_gate_loop(m, x_dev, sigmas_host, n_steps, text_dev, mode, gate, forced,
+                                    m->cap);
     m->capturing = false;
     hipGraph_t g = nullptr;
     const hipError_t e = hipStreamEndCapture(m->cap, &g);
@@ -1148,7 +1272,7 @@ acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev, const float* si
   }
   ACID_HIP(hipGraphLaunch(m->gexec, stream));
   if (trace) {
-    if (mode == ACID_MODE_ACID) {
+    if (mode != ACID_MODE_NOCACHE) {
       ACID_HIP(hipMemcpyAsync(trace, m->kp(m->kl.dtrace), n_steps * sizeof(acid_step_trace),
                               hipMemcpyDeviceToHost, stream));
       ACID_HIP(hipStreamSynchronize(stream));

@@ -7,7 +7,8 @@ the device (every model kernel predicated on the step's decision word,
 captured once and replayed) is checked bit for bit against the host-gated
 loop, over several replays with other eager work and synchronisations in
 between, after recaptures, under a forced schedule and without the cache,
-and once directly against the oracle's loop.
+and once directly against the oracle's loop; the same for EasyCache's and
+DiCache's signals under the device gate.
 """
 import math
 import os
@@ -211,9 +212,54 @@ def test_graph_loop_vs_oracle(P):
     assert rel_err(to_np(x), xr) < 1e-4
 
 
-def test_graph_loop_rejects_other_signals(P):
-    cfg = ai.TINY
+TINY3 = ai.TINY.replace(name="tiny3", n_blocks=3)
+
+
+def _signal_scale(m, x0, sig, td, mode):
+    """Median finite signal of an all-compute run (the thresholds' scale)."""
+    tr = m.denoise_loop(to_dev(x0), sig, td, mode=mode, tau_low=0.0, tau_high=0.0, delta=0.0)
+    s = tr["s"][np.isfinite(tr["s"])]
+    return float(np.median(s))
+
+
+@pytest.mark.parametrize("cfg,mode,probe", [(ai.TINY, "easycache", 0), (SMALL_BF16, "easycache", 0),
+                                            (TINY3, "dicache", 1), (TINY3, "dicache", 2),
+                                            (SMALL_BF16, "dicache", 1)],
+                         ids=["tiny-easycache", "bf16-easycache", "tiny3-dicache1",
+                              "tiny3-dicache2", "bf16-dicache1"])
+def test_graph_loop_other_signals_bit_exact(P, cfg, mode, probe):
+    """EasyCache's and DiCache's signals under the device gate: the captured
+    loop equals the host-gated loop bit for bit (x_N and trace), replayed
+    with other eager work between replays."""
     m, _, x0, td, sig = _loop_case(P, cfg)
-    for mode in ("easycache", "dicache"):
-        with pytest.raises(P.AcidError):
-            m.denoise_loop(to_dev(x0), sig, td, mode=mode, graph=True)
+    if mode == "dicache":
+        m.set_probe_blocks(probe)
+    sc = _signal_scale(m, x0, sig, td, mode)
+    if mode == "easycache":
+        gate = dict(tau_low=1.5 * sc, tau_high=3.0 * sc, delta=0.05 * sc)
+    else:
+        gate = dict(tau_low=1.2 * sc, tau_high=2.5 * sc, delta=0.05 * sc)
+    xe = to_dev(x0)
+    tre = m.denoise_loop(xe, sig, td, mode=mode, **gate)
+    assert 0 < tre["compute"].sum() < cfg.n_steps
+    x0d = to_dev(x0)
+    xg = to_dev(x0)
+    for rep in range(3):
+        if rep:
+            m.denoise_loop(to_dev(x0), sig, td, mode="acid", tau_low=0.05, tau_high=0.2, delta=0.01)
+            torch.cuda.synchronize()
+            xg.copy_(x0d)
+        trg = m.denoise_loop(xg, sig, td, mode=mode, **gate, graph=True)
+        torch.cuda.synchronize()
+        assert _same_trace(trg, tre), rep
+        assert torch.equal(xg, xe), rep
+    # a forced schedule through the captured loop
+    forced = np.zeros(cfg.n_steps, np.uint8)
+    forced[:2] = 1
+    forced[4::3] = 1
+    xf, xfg = to_dev(x0), to_dev(x0)
+    trf = m.denoise_loop(xf, sig, td, mode=mode, **gate, forced_schedule=forced)
+    trfg = m.denoise_loop(xfg, sig, td, mode=mode, **gate, forced_schedule=forced, graph=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(trfg["compute"], forced) and _same_trace(trfg, trf)
+    assert torch.equal(xfg, xf)
