@@ -255,6 +255,9 @@ def main() -> int:
                          "on the device, the loop captured once as a HIP graph and replayed")
     ap.add_argument("--graph-context", action="store_true",
                     help="also time the other loop variant (host gate / captured graph)")
+    ap.add_argument("--attention-context", action="store_true",
+                    help="also time PyTorch's scaled_dot_product_attention (flash backend only) "
+                         "at the workload's attention shape, as context")
     ap.add_argument("--no-nocache", action="store_true", help="skip the uncached context loop")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="disable the per-kernel event timer")
@@ -445,6 +448,31 @@ def main() -> int:
         nocache = time.perf_counter() - t1
         log(f"uncached loop: {nocache:.3f} s ({N} computed steps)")
 
+    library_attention = None
+    if args.attention_context and cfg.dtype == "bf16":
+        from torch.nn.attention import SDPBackend, sdpa_kernel
+        L, nh, d = cfg.n_tokens, cfg.n_heads, cfg.head_dim
+        g = torch.Generator(device="cuda")
+        g.manual_seed(7)
+        q, k, v = (torch.randn((1, nh, L, d), generator=g, device="cuda").to(torch.bfloat16)
+                   for _ in range(3))
+        try:
+            # flash backend only: no silent fallback to the batched-matmul path
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+                torch.nn.functional.scaled_dot_product_attention(q, k, v)
+                torch.cuda.synchronize()
+                t1 = time.perf_counter()
+                for _ in range(3):
+                    torch.nn.functional.scaled_dot_product_attention(q, k, v)
+                torch.cuda.synchronize()
+            ms = (time.perf_counter() - t1) / 3 * 1e3
+            library_attention = {"backend": "torch sdpa (flash)", "ms": ms,
+                                 "tflops": 4.0 * L * L * nh * d / (ms * 1e-3) / 1e12}
+        except RuntimeError as e:
+            library_attention = {"backend": "torch sdpa (flash)", "unavailable": str(e)[:200]}
+        del q, k, v
+        log(f"library attention: {library_attention}")
+
     cpu = None
     if not args.no_cpu_baseline:
         try:
@@ -496,6 +524,7 @@ def main() -> int:
         "nocache_s_per_loop": nocache,
         "speedup_vs_nocache": (nocache / s_per_loop) if nocache else None,
         "roofline": roofline,
+        **({"library_attention": library_attention} if library_attention else {}),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
