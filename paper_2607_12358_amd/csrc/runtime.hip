@@ -957,10 +957,11 @@ acid_status acid_model_load_tensor(acid_model* m, int32_t id, const float* src_d
 
 void acid_model_destroy(acid_model* m) {
   if (!m) return;
-  harvest(m);
-  for (auto e : m->pool) hipEventDestroy(e);
-  if (m->gexec) hipGraphExecDestroy(m->gexec);
-  if (m->cap) hipStreamDestroy(m->cap);
+  // teardown: errors here have nowhere to go
+  (void)harvest(m);
+  for (auto e : m->pool) (void)hipEventDestroy(e);
+  if (m->gexec) (void)hipGraphExecDestroy(m->gexec);
+  if (m->cap) (void)hipStreamDestroy(m->cap);
   delete m;
 }
 
@@ -1259,11 +1260,11 @@ acid_status acid_denoise_loop_graph(acid_model* m, float* x_dev, const float* si
     hipGraph_t g = nullptr;
     const hipError_t e = hipStreamEndCapture(m->cap, &g);
     if (st != ACID_OK || e != hipSuccess) {
-      if (g) hipGraphDestroy(g);
+      if (g) (void)hipGraphDestroy(g);
       return st != ACID_OK ? st : check_hip(e, "hipStreamEndCapture");
     }
     const hipError_t ei = hipGraphInstantiate(&m->gexec, g, nullptr, nullptr, 0);
-    hipGraphDestroy(g);
+    (void)hipGraphDestroy(g);
     if (ei != hipSuccess) {
       m->gexec = nullptr;
       return check_hip(ei, "hipGraphInstantiate");

@@ -17,6 +17,7 @@ struct SigmaPack {
 
 __global__ void sinusoid_kernel(SigmaPack sig, int n, int freq_dim, float* __restrict__ e) {
   const int i = blockIdx.x;
+  if (i >= n) return;
   const int half = freq_dim / 2;
   const double t = 1000.0 * (double)sig.v[i];
   const double lnp = 9.210340371976184;  // ln(10000)
