@@ -251,6 +251,19 @@ def test_denoise_loop_wan_fullsize_properties(P):
     tri = m.denoise_loop(xi, sig, mode="easycache", tau_low=math.inf, tau_high=math.inf,
                          delta=0.01)
     assert list(tri["compute"]) == [1, 1] + [0] * (cfg.n_steps - 2)
+    # DiCache's probe signal: the gate replays it, and the captured device-gate
+    # loop gives the same bits as the host-gated one
+    m.set_probe_blocks(1)
+    xd = x0.clone()
+    trd = m.denoise_loop(xd, sig, mode="dicache", tau_low=0.07, tau_high=0.225, delta=0.01)
+    dec, _, _ = O.gate_schedule(list(trd["s"]), O.GateParams(0.07, 0.225, 0.01))
+    assert list(trd["gate_compute"].astype(bool)) == dec
+    assert 0 < trd["compute"].sum() < cfg.n_steps
+    xdg = x0.clone()
+    trdg = m.denoise_loop(xdg, sig, mode="dicache", tau_low=0.07, tau_high=0.225, delta=0.01,
+                          graph=True)
+    assert torch.equal(xdg, xd) and np.array_equal(trdg["compute"], trd["compute"])
+    assert np.array_equal(trdg["s"][1:], trd["s"][1:])
 
 
 def test_denoise_loop_small_bf16_vs_oracle(P):
