@@ -260,7 +260,8 @@ acid_status acid_model_set_probe_blocks(acid_model* m, int32_t n_probe);
  * out_host[0] = sum |a - b| (sum |a| if b_dev is NULL), out_host[1] =
  * sum |c| (0 if c_dev is NULL).  fp64 accumulation in a fixed order
  * (deterministic).  Uses the model's workspace for partial sums, so n must
- * be at most n_video * hidden.  Synchronises the stream. */
+ * be at most n_video * hidden.  Synchronises the stream.  n == 0 gives
+ * (0, 0) without touching the buffers (which may then be NULL). */
 acid_status acid_l1_norms(acid_model* m, const float* a_dev, const float* b_dev,
                           const float* c_dev, int64_t n, double* out_host,
                           hipStream_t stream);

@@ -1094,15 +1094,16 @@ acid_status acid_model_set_probe_blocks(acid_model* m, int32_t n_probe) {
 
 acid_status acid_l1_norms(acid_model* m, const float* a_dev, const float* b_dev,
                           const float* c_dev, int64_t n, double* out_host, hipStream_t stream) {
-  if (!m || !a_dev || !out_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (!m || !out_host) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
   if (n < 0 || n > m->Lv() * m->H())
     return set_error(ACID_ERR_INVALID_ARG, "n %lld outside [0, n_video * hidden]", (long long)n);
-  if (((uintptr_t)a_dev | (uintptr_t)b_dev | (uintptr_t)c_dev) % 16)
-    return set_error(ACID_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
-  if (n == 0) {
+  if (n == 0) {  // empty sums; the buffers are not touched
     out_host[0] = out_host[1] = 0.0;
     return ACID_OK;
   }
+  if (!a_dev) return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
+  if (((uintptr_t)a_dev | (uintptr_t)b_dev | (uintptr_t)c_dev) % 16)
+    return set_error(ACID_ERR_INVALID_ARG, "buffers must be 16-byte aligned");
   return l1_norms(m, a_dev, b_dev, c_dev, n, out_host, stream);
 }
 

@@ -13,7 +13,7 @@ import torch
 
 import acid_inputs as ai
 import oracle as O
-from gpu_util import bf16_values, need_gpu, rel_err, to_dev, to_np
+from gpu_util import bf16_values, make_model, need_gpu, rel_err, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -240,3 +240,25 @@ def test_linear_deterministic(P):
         (o, _, _), = _linear_case(P, "bias", 700, 1536, 1536, torch.bfloat16, seed=5)
         got.append(o)
     assert np.array_equal(got[0], got[1]) and np.array_equal(got[0], got[2])
+
+
+def test_empty_inputs_are_no_ops(P):
+    """Zero-length work through every component call returns cleanly and
+    writes nothing: attention over 0 tokens, a GEMM with 0 rows, the cache,
+    EasyCache's reuse and L1 sums over 0 elements."""
+    dev = "cuda"
+    for d in (64, 128):
+        q = torch.empty((2, 0, d), dtype=torch.bfloat16, device=dev)
+        vt = torch.empty((2, d, 0), dtype=torch.bfloat16, device=dev)
+        P.attention(q, q, vt, torch.empty((0, 2 * d), dtype=torch.bfloat16, device=dev))
+    wt = torch.zeros((256, 128), dtype=torch.bfloat16, device=dev)
+    b = torch.zeros(256, device=dev)
+    P.linear(torch.empty((0, 128), dtype=torch.bfloat16, device=dev), wt, P.ACID_EPI_BIAS, b,
+             out=torch.empty((0, 256), device=dev))
+    z = torch.empty(0, device=dev)
+    P.cache_apply(P.ACID_CACHE_STORE, z, z, z)
+    P.easycache_reuse(z, z, z, z, -0.1)
+    torch.cuda.synchronize()
+    m, _ = make_model(P, ai.TINY, max_steps=2)
+    x = torch.ones(4, device=dev)
+    assert m.l1_norms(x[:0], x[:0], x[:0]) == (0.0, 0.0)
