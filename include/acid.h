@@ -351,11 +351,16 @@ acid_status acid_ln_modulate(int32_t out_dtype, const float* x_dev,
  * head.  q, k: [n_heads][L][d]; vt: V transposed, [n_heads][d][vt_ld] with
  * vt_ld >= round_up(L, 8) (entries past L are ignored); o: [L][n_heads*d]
  * (token-major).  All in `dtype`; softmax statistics in fp32.  d is 64 or
- * 128. */
+ * 128.  q_prescaled 0: q holds Q; 1: q holds Q multiplied by
+ * log2(e)/sqrt(d) (the float value 1.4426950408889634f / sqrtf(d)) and
+ * rounded to `dtype`, as the QKV epilogue writes it with q_prescale set
+ * (the softmax then needs no per-score scaling); other values:
+ * ACID_ERR_INVALID_ARG. */
 acid_status acid_attention(int32_t dtype, int32_t n_heads, int64_t seq_len,
                            int32_t head_dim, const void* q_dev,
                            const void* k_dev, const void* vt_dev,
-                           int64_t vt_ld, void* o_dev, hipStream_t stream);
+                           int64_t vt_ld, void* o_dev, int32_t q_prescaled,
+                           hipStream_t stream);
 
 /* Epilogues of the fused GEMM y = a W + b (acc in fp32). */
 typedef enum {
@@ -385,6 +390,9 @@ typedef struct {
   int32_t n_heads;      /* QKV: N == 3 * n_heads * head_dim (QKV_GELU: >) */
   int32_t head_dim;     /* QKV */
   float dsigma;         /* EULER */
+  int32_t q_prescale;   /* QKV kinds: 1 stores Q multiplied by log2(e)/sqrt(
+                           head_dim) (see acid_attention's q_prescaled), 0
+                           plain Q; K and V are never scaled */
 } acid_epilogue_args;
 
 /* Fused GEMM: a [M][K] and wt = W transposed [N][K], both in `dtype`;

@@ -124,16 +124,25 @@ def ln_modulate(x, shift, scale, out, stream=None) -> None:
                                  _ptr(out), _stream(stream)))
 
 
-def attention(q, k, vt, o, stream=None) -> None:
-    """q, k [heads, L, d]; vt [heads, d, vt_ld]; o [L, heads*d]; all bf16 or all fp32."""
+def attention(q, k, vt, o, stream=None, q_prescaled: bool = False) -> None:
+    """q, k [heads, L, d]; vt [heads, d, vt_ld]; o [L, heads*d]; all bf16 or all fp32.
+    q_prescaled: q holds Q * q_scale(d), as the QKV epilogue stores it with
+    q_prescale=True (the model's own path)."""
     n_heads, L, d = q.shape
     code = ACID_BF16 if q.dtype == _torch().bfloat16 else ACID_F32
     check(lib().acid_attention(code, n_heads, L, d, _ptr(q), _ptr(k), _ptr(vt), vt.shape[2],
-                               _ptr(o), _stream(stream)))
+                               _ptr(o), int(bool(q_prescaled)), _stream(stream)))
+
+
+def q_scale(d: int) -> float:
+    """The float32 factor log2(e)/sqrt(d) a pre-scaled Q carries."""
+    import numpy as np
+    return float(np.float32(np.float32(1.4426950408889634) / np.sqrt(np.float32(d))))
 
 
 def linear(a, wt, kind: int, bias, gate=None, out=None, v_out=None, q=None, k=None, vt=None,
-           n_heads=0, head_dim=0, dsigma=0.0, bias2=None, stream=None) -> None:
+           n_heads=0, head_dim=0, dsigma=0.0, bias2=None, q_prescale=False,
+           stream=None) -> None:
     """Fused GEMM y = a @ wt.T + bias with an epilogue (see include/acid.h).
     For ACID_EPI_QKV_GELU, out may be a row-strided view (unit column
     stride); its row stride is passed as out_ld."""
@@ -156,6 +165,7 @@ def linear(a, wt, kind: int, bias, gate=None, out=None, v_out=None, q=None, k=No
     e.q, e.k, e.vt = _ptr(q), _ptr(k), _ptr(vt)
     e.vt_ld = vt.shape[-1] if vt is not None else 0
     e.n_heads, e.head_dim, e.dsigma = n_heads, head_dim, dsigma
+    e.q_prescale = int(bool(q_prescale))
     check(lib().acid_linear(code, M, N, K, _ptr(a), _ptr(wt), C.byref(e), _stream(stream)))
 
 

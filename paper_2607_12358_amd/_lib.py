@@ -61,7 +61,8 @@ class EpilogueArgsC(C.Structure):
                 ("bias2", C.c_void_p), ("out", C.c_void_p), ("out_ld", C.c_int64),
                 ("v_out", C.c_void_p), ("q", C.c_void_p),
                 ("k", C.c_void_p), ("vt", C.c_void_p), ("vt_ld", C.c_int64),
-                ("n_heads", C.c_int32), ("head_dim", C.c_int32), ("dsigma", C.c_float)]
+                ("n_heads", C.c_int32), ("head_dim", C.c_int32), ("dsigma", C.c_float),
+                ("q_prescale", C.c_int32)]
 
 
 _P = C.c_void_p
@@ -98,7 +99,7 @@ _SIGS = {
     "acid_timestep_modulation": (C.c_int, [_P, C.POINTER(C.c_float), C.c_int32, _P, _P]),
     "acid_ln_modulate": (C.c_int, [C.c_int32, _P, C.c_int64, C.c_int32, _P, _P, _P, _P]),
     "acid_attention": (C.c_int, [C.c_int32, C.c_int32, C.c_int64, C.c_int32, _P, _P, _P,
-                                 C.c_int64, _P, _P]),
+                                 C.c_int64, _P, C.c_int32, _P]),
     "acid_linear": (C.c_int, [C.c_int32, C.c_int64, C.c_int32, C.c_int32, _P, _P,
                               C.POINTER(EpilogueArgsC), _P]),
     "acid_block_forward": (C.c_int, [_P, C.c_int32, _P, _P, _P]),

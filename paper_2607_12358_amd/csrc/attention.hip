@@ -19,10 +19,13 @@
 //   through the probability sum).
 //   Work items are mapped so each XCD streams a contiguous, head-major range
 //   (a head's K/V passes through few L2s).  Softmax runs in the exp2 domain
-//   with log2(e)/sqrt(d) folded into one FMA per score, in fp32; the row sum
-//   adds the bf16-rounded probabilities that the P V product uses.
-// fp32 path: one thread per query with K/V tiles in LDS, online softmax in
-//   fp32 (for the fp32 configuration).
+//   in fp32: with plain Q, log2(e)/sqrt(d) is folded into one FMA per score;
+//   with Q stored pre-multiplied by log2(e)/sqrt(d) (as the model's QKV
+//   epilogue writes it) the score MFMAs start from -m and deliver the exp2
+//   arguments themselves.  The row sum adds the bf16-rounded probabilities
+//   that the P V product uses.
+// fp32 path: one wave per (head, query), online softmax in fp32 (for the
+//   fp32 configuration).
 #include "common.h"
 
 namespace acid {
@@ -107,7 +110,7 @@ __device__ __forceinline__ float half_swap_max(float v) {
 // depend on the order of the keys, so the ragged last tile (keys up to L)
 // is processed first, staged through registers and masked in the prologue;
 // every tile of the loop is full and arrives by DMA.
-template <int D, int NW>
+template <int D, int NW, bool kPre>
 __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* Q,
                                                            const bf16* Kp,
                                                            const bf16* Vt,
@@ -159,6 +162,14 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -__builtin_inff(), l_run = 0.f;
+  // kPre (Q stored pre-multiplied by log2(e)/sqrt(d)): the score MFMAs start
+  // from C = -m instead of 0, so they deliver the exp2 arguments directly and
+  // no per-score multiply-add remains.  cneg holds -m in every entry.
+  f32x16 cneg;
+  auto set_cneg = [&](float v) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) cneg[r] = v;
+  };
 
   // Offsets are 32-bit (a head's K is L * d elements, its V^T d * vt_ld:
   // far below 2^31 bytes).
@@ -228,10 +239,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
 
   // S^T (keys x queries) of the K tile in buffer kbuf, two 32-key blocks.
   auto scores = [&](f32x16(&s)[2], int kbuf) {
+    if constexpr (!kPre) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+        for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+    }
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk)
 #pragma unroll
@@ -239,7 +252,8 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         const int kr = kb * 32 + lr;
         const bf16x8 kf = *reinterpret_cast<const bf16x8*>(Ks + kbuf * Ld::K_ELEMS + kr * KLD +
                                                             swz<KCH>(kr, 2 * kk + lg) * 8);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk],
+                                                        (kPre && kk == 0) ? cneg : s[kb], 0, 0, 0);
       }
   };
   // Row max of the first (raw) score tile, shared with the partner half-wave
@@ -250,14 +264,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    m_run = half_swap_max(mx) * scale_log2;
+    m_run = kPre ? half_swap_max(mx) : half_swap_max(mx) * scale_log2;
   };
   // Scores to exp2 arguments in place: s log2(e)/sqrt(d) - m.
   auto shift = [&](f32x16(&s)[2]) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = __builtin_fmaf(s[kb][r], scale_log2, -m_run);
+      for (int r = 0; r < 16; ++r)
+        s[kb][r] = kPre ? s[kb][r] - m_run : __builtin_fmaf(s[kb][r], scale_log2, -m_run);
+  };
+  auto sub_all = [&](f32x16(&s)[2], float v) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] -= v;
   };
   // Row max of a raw score tile (scale > 0 commutes with max), shared with
   // the partner half-wave that holds the other keys of the same query, then
@@ -265,7 +286,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   // Lazy rescaling: the reference max m moves only when the new max exceeds
   // it by more than 2^8 in probability, so probabilities stay <= 256 (exact
   // range for bf16 and fp32) and the O / l rescale is skipped on most tiles.
-  float m_nx = 0.f, a_nx = 1.f;
+  float m_nx = 0.f, a_nx = 1.f, d_nx = 0.f;
   bool g_nx = false;
   auto row_max_shift = [&](f32x16(&s)[2]) {
     float mx = s[0][0];
@@ -282,6 +303,20 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[kb][r] = __builtin_fmaf(s[kb][r], scale_log2, -m_nx);
+  };
+  // kPre: the tile already holds s' - m; only the lazy-rescale decision is
+  // taken here (its shift by d_nx, rare, is applied at the next iteration).
+  auto row_max_check = [&](const f32x16(&s)[2]) {
+    float mx = s[0][0];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+    mx = half_swap_max(mx);
+    g_nx = mx > 8.0f;
+    d_nx = g_nx ? mx : 0.0f;
+    m_nx = m_run + d_nx;
+    a_nx = __builtin_amdgcn_exp2f(-d_nx);
   };
   // p = 2^(shifted score), rounded to bf16 as the B operand of the P V
   // MFMAs; the row sum adds exactly those bf16 values (v_dot2 with (1, 1)).
@@ -304,6 +339,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         pf[kb][k2] = __builtin_bit_cast(bf16x8, w);
       }
     psum = ps[0] + ps[1];
+  };
+  // The same for the 16 keys of one P V K-step (kb, k2) only, adding into ps.
+  auto probs_part = [&](const f32x16(&s)[2], int kb, int k2, bf16x8(&pf)[2][2],
+                        float(&ps)[2]) {
+    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = 8 * k2 + 2 * e;
+      const bf16x2 pr = {(bf16)__builtin_amdgcn_exp2f(s[kb][r]),
+                         (bf16)__builtin_amdgcn_exp2f(s[kb][r + 1])};
+      ps[e & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps[e & 1], false);
+      w[e] = __builtin_bit_cast(uint32_t, pr);
+    }
+    pf[kb][k2] = __builtin_bit_cast(bf16x8, w);
   };
   // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
   // (kb, k2) is S^T row kb*32 + 16 k2 + 8 (e/4) + 4 lg + e%4, i.e. key
@@ -353,11 +403,53 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         for (int db = 0; db < ND; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[db][r] *= a_nx;
+        if constexpr (kPre) {
+          sub_all(sc, d_nx);
+          set_cneg(-m_run);
+        }
       }
       __builtin_amdgcn_sched_barrier(0);
     }
     bf16x8 pf[2][2];
     float psum;
+    if constexpr (kPre && !kOptimistic) {
+      // The exponentials of the first key block under the score MFMAs of the
+      // next tile, those of the second under the first half of the P V
+      // MFMAs (which use only the first block), the row max of the next
+      // tile under the second half; exponentials (transcendental unit) and
+      // the other VALU work in separate groups, one or two of each per MFMA.
+      float ps[2] = {0.f, 0.f};
+      probs_part(sc, 0, 0, pf, ps);
+      probs_part(sc, 0, 1, pf, ps);
+      scores(sn, (it + 1) & 1);
+      probs_part(sc, 1, 0, pf, ps);
+      probs_part(sc, 1, 1, pf, ps);
+      psum = ps[0] + ps[1];
+      l_run += psum;
+      pv(pf, it & 1);
+      row_max_check(sn);
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int i = 0; i < 2 * NK; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x400, (16 + 2 * NK - 1) / (2 * NK), 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, (16 + 2 * NK - 1) / (2 * NK), 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 2 * ND; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x400, (16 + 2 * ND - 1) / (2 * ND), 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, (18 + 2 * ND - 1) / (2 * ND), 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 2 * ND; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, (24 + 2 * ND - 1) / (2 * ND), 0);
+      }
+    } else {
     probs(sc, pf, psum);
     scores(sn, (it + 1) & 1);
     if constexpr (kOptimistic) {
@@ -386,22 +478,25 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         for (int db = 0; db < ND; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sc[kb][r] -= d;
+        sub_all(sc, d);
+        if constexpr (kPre) {
+          sub_all(sn, d);  // formed against the old reference
+          set_cneg(-m_run);
+        }
         probs(sc, pf, psum);
       }
       __builtin_amdgcn_sched_barrier(0);
       l_run += psum;
       pv(pf, it & 1);
-      shift(sn);
-      // Each P V MFMA with one fragment read and a share of the shift.
+      if constexpr (!kPre) {
+        shift(sn);
+        // Each P V MFMA with one fragment read and a share of the shift.
 #pragma unroll
-      for (int i = 0; i < 4 * ND; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, (32 + 4 * ND - 1) / (4 * ND), 0);
+        for (int i = 0; i < 4 * ND; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, (32 + 4 * ND - 1) / (4 * ND), 0);
+        }
       }
     } else {
       l_run += psum;
@@ -424,6 +519,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         __builtin_amdgcn_sched_group_barrier(0x002, (56 + 4 * ND - 1) / (4 * ND), 0);
       }
     }
+    }
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);  // this iteration's staging has landed
     __builtin_amdgcn_s_barrier();
@@ -439,6 +535,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   if (nkv > 1) stage_k_dma(1, (1 - has_tail) * BKV);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  if constexpr (kPre) set_cneg(0.0f);
   scores(sa, 0);
   if (has_tail) {
     // Keys past L get score -inf.  S^T row kb*32 + 8 (r/4) + 4 lg + r%4
@@ -452,7 +549,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         if (key >= Li) sa[kb][r] = -__builtin_inff();
       }
   }
-  if constexpr (kOptimistic) {
+  if constexpr (kPre) {
+    // The first reference is the first tile's row max (held against m = 0).
+    first_max(sa);
+    sub_all(sa, m_run);
+    set_cneg(-m_run);
+    m_nx = m_run;
+  } else if constexpr (kOptimistic) {
     first_max(sa);
     shift(sa);
   } else {
@@ -533,9 +636,9 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
       s = a * scale;
     }
     const float m_new = fmaxf(m_run, wave_max(s));  // finite: the chunk has a key
-    const float alpha = expf(m_run - m_new);
+    const float alpha = exp2f(m_run - m_new);
     m_run = m_new;
-    const float p = j < L ? expf(s - m_new) : 0.f;
+    const float p = j < L ? exp2f(s - m_new) : 0.f;
     l_run = l_run * alpha + wave_sum(p);
 #pragma unroll
     for (int c = 0; c < C; ++c) o[c] *= alpha;
@@ -554,7 +657,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__
 
 // Waves per workgroup: 8 for d = 128 (a staged K/V tile feeds 256 queries),
 // 4 for d = 64 (finer grid for the shorter sequences of that configuration).
-template <int D>
+template <int D, bool kPre>
 hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
                        int64_t vt_ld, void* o, int64_t o_ld, hipStream_t s,
                        const int32_t* pred) {
@@ -562,15 +665,15 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
   constexpr int BQ = 32 * NW;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute((const void*)attn_bf16_kernel<D, NW>,
+    hipError_t err = hipFuncSetAttribute((const void*)attn_bf16_kernel<D, NW, kPre>,
                                          hipFuncAttributeMaxDynamicSharedMemorySize,
                                          (int)AttnLds<D>::BYTES);
     if (err != hipSuccess) return err;
     attr_set = true;
   }
-  const float scale_log2 = 1.4426950408889634f / sqrtf((float)D);
+  const float scale_log2 = attn_q_scale(D);
   dim3 grid((unsigned)(((L + BQ - 1) / BQ) * n_heads));
-  hipLaunchKernelGGL((attn_bf16_kernel<D, NW>), grid, dim3(64 * NW), AttnLds<D>::BYTES, s,
+  hipLaunchKernelGGL((attn_bf16_kernel<D, NW, kPre>), grid, dim3(64 * NW), AttnLds<D>::BYTES, s,
                      (const bf16*)q, (const bf16*)k, (const bf16*)vt, L, vt_ld, n_heads,
                      (bf16*)o, o_ld, scale_log2, pred);
   return hipGetLastError();
@@ -578,11 +681,12 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
 
 template <int D>
 hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, const void* vt,
-                      int64_t vt_ld, void* o, int64_t o_ld, hipStream_t s, const int32_t* pred) {
+                      int64_t vt_ld, void* o, int64_t o_ld, hipStream_t s, const int32_t* pred,
+                      bool q_prescaled) {
   dim3 grid((unsigned)((L * n_heads + 3) / 4));
   hipLaunchKernelGGL(attn_f32_kernel<D>, grid, dim3(256), 0, s, (const float*)q,
                      (const float*)k, (const float*)vt, L, vt_ld, n_heads, (float*)o, o_ld,
-                     1.0f / sqrtf((float)D), pred);
+                     q_prescaled ? 1.0f : attn_q_scale(D), pred);
   return hipGetLastError();
 }
 
@@ -590,15 +694,20 @@ hipError_t launch_f32(int n_heads, int64_t L, const void* q, const void* k, cons
 
 hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
                             const void* k, const void* vt, int64_t vt_ld, void* o,
-                            hipStream_t s, const int32_t* pred, int64_t o_ld) {
+                            hipStream_t s, const int32_t* pred, int64_t o_ld,
+                            bool q_prescaled) {
   if (L == 0) return hipSuccess;
   if (o_ld == 0) o_ld = (int64_t)n_heads * d;
   if (dtype == ACID_BF16) {
-    if (d == 64) return launch_bf16<64>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
-    if (d == 128) return launch_bf16<128>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
+    if (d == 64)
+      return q_prescaled ? launch_bf16<64, true>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred)
+                         : launch_bf16<64, false>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
+    if (d == 128)
+      return q_prescaled ? launch_bf16<128, true>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred)
+                         : launch_bf16<128, false>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
   } else {
-    if (d == 64) return launch_f32<64>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
-    if (d == 128) return launch_f32<128>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred);
+    if (d == 64) return launch_f32<64>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred, q_prescaled);
+    if (d == 128) return launch_f32<128>(n_heads, L, q, k, vt, vt_ld, o, o_ld, s, pred, q_prescaled);
   }
   return hipErrorInvalidValue;
 }

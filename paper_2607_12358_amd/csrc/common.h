@@ -64,6 +64,11 @@ __device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
 
 inline int64_t round_up(int64_t a, int64_t b) { return (a + b - 1) / b * b; }
 
+// log2(e) / sqrt(d): the factor that turns a dot product q.k into the
+// softmax's exp2 argument.  Attention with plain Q applies it per score; the
+// QKV epilogue can store Q pre-multiplied by it (the same float value).
+inline float attn_q_scale(int d) { return 1.4426950408889634f / sqrtf((float)d); }
+
 // ---------------------------------------------------------------- launchers
 // Each returns hipGetLastError() of its launch.
 
@@ -130,6 +135,7 @@ hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, cons
 // o_ld: row stride of O in elements (0: n_heads * d).
 hipError_t launch_attention(int dtype, int n_heads, int64_t L, int d, const void* q,
                             const void* k, const void* vt, int64_t vt_ld, void* o,
-                            hipStream_t s, const int32_t* pred = nullptr, int64_t o_ld = 0);
+                            hipStream_t s, const int32_t* pred = nullptr, int64_t o_ld = 0,
+                            bool q_prescaled = false);
 
 }  // namespace acid

@@ -45,6 +45,7 @@ struct Epi {
   const float* bias2;   // GATE_RESIDUAL: optional second bias
   int64_t out_ld;       // QKV_GELU: row stride of the GELU output
   int n_qkv;            // QKV_GELU: columns [0, n_qkv) are Q | K | V
+  float q_mul;          // QKV kinds: factor on the Q columns (1: plain Q)
 };
 
 // Q | K | V head-major destination of column c < 3 H (which = c / H).
@@ -77,7 +78,7 @@ __device__ __forceinline__ void epi_elem(const Epi& e, int64_t m, int n, int N, 
     if (KIND == ACID_EPI_QKV || n < e.n_qkv) {
       int64_t stride;
       T* dst = qkv_dst<T>(e, n, stride);
-      dst[m * stride] = (T)y;
+      dst[m * stride] = (T)(n < e.H ? y * e.q_mul : y);
     } else {
       static_cast<T*>(e.out)[m * e.out_ld + (n - e.n_qkv)] = (T)gelu_tanh(y);
     }
@@ -99,6 +100,7 @@ struct ColEpi {
   int64_t stride;
   float dsigma;
   bool gelu;  // QKV_GELU: this column is in the GELU part
+  float qmul;  // QKV kinds: e.q_mul on the Q columns, else 1
   __device__ __forceinline__ ColEpi(const Epi& e, int n, int N) {
     bias = e.bias[n];
     if (KIND == ACID_EPI_GATE_RESIDUAL && e.bias2) bias += e.bias2[n];
@@ -109,6 +111,7 @@ struct ColEpi {
     v_f = nullptr;
     stride = N;
     gelu = false;
+    qmul = ((KIND == ACID_EPI_QKV || KIND == ACID_EPI_QKV_GELU) && n < e.H) ? e.q_mul : 1.f;
     if constexpr (KIND == ACID_EPI_QKV) {
       dst_t = qkv_dst<T>(e, n, stride);
     } else if constexpr (KIND == ACID_EPI_QKV_GELU) {
@@ -156,9 +159,9 @@ struct ColEpi {
       float* h = dst_f + m * stride;
       *h = *h + gate * y;
     } else if constexpr (KIND == ACID_EPI_QKV) {
-      dst_t[m * stride] = (T)y;
+      dst_t[m * stride] = (T)(y * qmul);
     } else if constexpr (KIND == ACID_EPI_QKV_GELU) {
-      float z = y;
+      float z = y * qmul;
       if (gelu) {
         if constexpr (sizeof(T) == 2)
           z = gelu_tanh_fast(y);
@@ -532,6 +535,7 @@ hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, cons
   e.bias2 = ea.bias2;
   e.out_ld = ea.out_ld;
   e.n_qkv = 3 * ea.n_heads * ea.head_dim;
+  e.q_mul = ea.q_prescale ? attn_q_scale(ea.head_dim) : 1.f;
   switch (ea.kind) {
     case ACID_EPI_BIAS: return launch_kind<ACID_EPI_BIAS>(dtype, M, N, K, a, wt, e, s);
     case ACID_EPI_BIAS_GELU: return launch_kind<ACID_EPI_BIAS_GELU>(dtype, M, N, K, a, wt, e, s);

@@ -325,11 +325,13 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   e.vt_ld = m->kl.vt_ld;
   e.n_heads = c.n_heads;
   e.head_dim = c.head_dim;
+  e.q_prescale = 1;  // Q leaves the GEMM in the softmax's exp2 units
   ACID_TRY(run(m, ACID_K_GEMM_QKV, s, "qkv gemm", [&]() {
     return launch_linear(dt, L, 3 * H, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred);
   }));
   ACID_TRY(run(m, ACID_K_ATTENTION, s, "attention", [&]() {
-    return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, o, s, pred);
+    return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, o, s, pred, 0,
+                            true);
   }));
   acid_epilogue_args p = {};
   p.kind = ACID_EPI_GATE_RESIDUAL;
@@ -382,12 +384,13 @@ acid_status block_forward_parallel(acid_model* m, int b, const float* mod6, floa
   e.head_dim = c.head_dim;
   e.out = g + (size_t)H * esize(dt);
   e.out_ld = H + F;
+  e.q_prescale = 1;
   ACID_TRY(run(m, ACID_K_GEMM_QKV, s, "qkv+mlp gemm", [&]() {
     return launch_linear(dt, L, 3 * H + F, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred);
   }));
   ACID_TRY(run(m, ACID_K_ATTENTION, s, "attention", [&]() {
     return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, g, s, pred,
-                            H + F);
+                            H + F, true);
   }));
   acid_epilogue_args p = {};
   p.kind = ACID_EPI_GATE_RESIDUAL;
@@ -1016,9 +1019,12 @@ acid_status acid_ln_modulate(int32_t out_dtype, const float* x_dev, int64_t rows
 
 acid_status acid_attention(int32_t dtype, int32_t n_heads, int64_t seq_len, int32_t head_dim,
                            const void* q_dev, const void* k_dev, const void* vt_dev,
-                           int64_t vt_ld, void* o_dev, hipStream_t stream) {
+                           int64_t vt_ld, void* o_dev, int32_t q_prescaled,
+                           hipStream_t stream) {
   if (dtype != ACID_F32 && dtype != ACID_BF16)
     return set_error(ACID_ERR_INVALID_ARG, "bad dtype %d", dtype);
+  if (q_prescaled != 0 && q_prescaled != 1)
+    return set_error(ACID_ERR_INVALID_ARG, "q_prescaled %d: 0 or 1", q_prescaled);
   if (n_heads < 1 || seq_len < 0) return set_error(ACID_ERR_INVALID_ARG, "n_heads < 1 or seq_len < 0");
   if (head_dim != 64 && head_dim != 128)
     return set_error(ACID_ERR_SHAPE, "head_dim %d: supported 64 or 128", head_dim);
@@ -1028,7 +1034,7 @@ acid_status acid_attention(int32_t dtype, int32_t n_heads, int64_t seq_len, int3
   if (seq_len > 0 && (!q_dev || !k_dev || !vt_dev || !o_dev))
     return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
   hipError_t e = launch_attention(dtype, n_heads, seq_len, head_dim, q_dev, k_dev, vt_dev, vt_ld,
-                                  o_dev, stream);
+                                  o_dev, stream, nullptr, 0, q_prescaled != 0);
   return e == hipSuccess ? ACID_OK : check_hip(e, "attention");
 }
 
@@ -1037,6 +1043,8 @@ acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K, const vo
   if (dtype != ACID_F32 && dtype != ACID_BF16)
     return set_error(ACID_ERR_INVALID_ARG, "bad dtype %d", dtype);
   if (!epi) return set_error(ACID_ERR_INVALID_ARG, "epilogue args NULL");
+  if (epi->q_prescale != 0 && epi->q_prescale != 1)
+    return set_error(ACID_ERR_INVALID_ARG, "q_prescale %d: 0 or 1", epi->q_prescale);
   if (M < 0 || N <= 0 || K <= 0) return set_error(ACID_ERR_INVALID_ARG, "bad M/N/K");
   if (N % 128 || K % 128)
     return set_error(ACID_ERR_SHAPE, "N %d and K %d must be multiples of 128", N, K);

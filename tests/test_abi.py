@@ -68,6 +68,20 @@ def test_null_arguments_rejected(lib):
     assert lib.acid_cache_apply(0, None, None, None, 0, None) == 0  # empty is a no-op
 
 
+def test_prescaled_q_flags_checked(lib):
+    """q_prescaled / q_prescale take 0 or 1; checked before any GPU work."""
+    assert lib.acid_attention(L.ACID_BF16, 2, 0, 128, None, None, None, 0, None, 2,
+                              None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_attention(L.ACID_BF16, 2, 0, 128, None, None, None, 0, None, 1, None) == 0
+    e = L.EpilogueArgsC()
+    e.kind = L.ACID_EPI_QKV
+    e.q_prescale = 2
+    assert lib.acid_linear(L.ACID_BF16, 0, 384, 128, None, None, C.byref(e),
+                           None) == L.ACID_ERR_INVALID_ARG
+    e.q_prescale = 1
+    assert lib.acid_linear(L.ACID_BF16, 0, 384, 128, None, None, C.byref(e), None) == 0
+
+
 def test_device_gate_and_graph_loop_argument_errors(lib):
     """Argument checks that return before any GPU work."""
     pc = L.GateParamsC(0.05, 0.2, 0.01, 1)

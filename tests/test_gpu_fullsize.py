@@ -34,23 +34,32 @@ def _seeded(shape, seed, std=1.0, dtype=torch.bfloat16):
 ATTN_SHAPES = [(12, 32760, 128), (48, 17776, 64), (24, 119056, 128)]
 
 
+@pytest.mark.parametrize("prescaled", [False, True], ids=["plain-q", "prescaled-q"])
 @pytest.mark.parametrize("nh,L,d", ATTN_SHAPES, ids=["wan", "cogvideox", "hunyuan"])
-def test_attention_fullsize_sampled(P, nh, L, d):
+def test_attention_fullsize_sampled(P, nh, L, d, prescaled):
+    """Sampled rows at the workloads' full sizes; prescaled-q is the launch
+    configuration of the model's loop (Q stored times log2(e)/sqrt(d))."""
     q = _seeded((nh, L, d), 1)
+    c = np.float32(P.q_scale(d))
+    if prescaled:
+        q = (q.float() * float(c)).to(torch.bfloat16)
     k = _seeded((nh, L, d), 2)
     v = _seeded((nh, L, d), 3)
     vt_ld = (L + 7) // 8 * 8
     vt = torch.zeros((nh, d, vt_ld), dtype=torch.bfloat16, device="cuda")
     vt[:, :, :L] = v.transpose(1, 2)
     o = torch.empty((L, nh * d), dtype=torch.bfloat16, device="cuda")
-    P.attention(q, k, vt, o)
+    P.attention(q, k, vt, o, q_prescaled=prescaled)
     torch.cuda.synchronize()
     rng = np.random.default_rng(L)
     heads = sorted(rng.choice(nh, 3, replace=False))
     rows = np.unique(np.concatenate([rng.choice(L, 40, replace=False), [0, L - 1]]))
     for j in heads:
         kj, vj = to_np(k[j]), to_np(v[j])
-        ref = O.attention(to_np(q[j])[rows], kj, vj)
+        qj = to_np(q[j])[rows].astype(np.float64)
+        if prescaled:
+            qj = qj / np.float64(c)
+        ref = O.attention(qj, kj, vj)
         got = to_np(o[rows, j * d:(j + 1) * d])
         assert rel_err(got, ref) < 1e-2, (j, rel_err(got, ref))
 

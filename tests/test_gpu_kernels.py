@@ -68,29 +68,46 @@ def test_ln_modulate(P, rows, H, out):
 # -------------------------------------------------------------- attention
 
 
-def _attn_case(P, n_heads, L, d, dtype, std, seed):
+def prescale_q(P, q, d, dtype):
+    """Q as the model's QKV epilogue stores it for attention with
+    q_prescaled: the float32 product with log2(e)/sqrt(d), rounded once to
+    the storage type.  Returns the stored values and the Q they stand for
+    (stored / factor, in float64), the input of the attention definition."""
+    c = np.float32(P.q_scale(d))
+    stored = (q.astype(np.float32) * c).astype(np.float32)
+    if dtype == torch.bfloat16:
+        stored = bf16_values(stored)
+    return stored, stored.astype(np.float64) / np.float64(c)
+
+
+def _attn_case(P, n_heads, L, d, dtype, std, seed, prescaled=False):
     rng = np.random.default_rng(seed)
     q = rng.normal(size=(n_heads, L, d)).astype(np.float32) * std
     k = rng.normal(size=(n_heads, L, d)).astype(np.float32) * std
     v = rng.normal(size=(n_heads, L, d)).astype(np.float32)
     if dtype == torch.bfloat16:
         q, k, v = bf16_values(q), bf16_values(k), bf16_values(v)
+    q_dev = q
+    if prescaled:
+        q_dev, q = prescale_q(P, q, d, dtype)
     vt_ld = ((L + 7) // 8) * 8
     vt = np.zeros((n_heads, d, vt_ld), np.float32)
     vt[:, :, :L] = v.transpose(0, 2, 1)
     vt[:, :, L:] = np.nan  # padding must never reach the output
     o = torch.empty((L, n_heads * d), dtype=dtype, device="cuda")
-    P.attention(to_dev(q, dtype), to_dev(k, dtype), to_dev(vt, dtype), o)
+    P.attention(to_dev(q_dev, dtype), to_dev(k, dtype), to_dev(vt, dtype), o, q_prescaled=prescaled)
     torch.cuda.synchronize()
     return q, k, v, to_np(o)
 
 
+@pytest.mark.parametrize("prescaled", [False, True], ids=["plain-q", "prescaled-q"])
 @pytest.mark.parametrize("L", [1, 63, 64, 65, 130, 300, 1000])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("std", [1.0, 4.0])
-def test_attention_bf16(P, L, d, std):
+def test_attention_bf16(P, L, d, std, prescaled):
     nh = 2
-    q, k, v, o = _attn_case(P, nh, L, d, torch.bfloat16, std, seed=L * 131 + d + int(std))
+    q, k, v, o = _attn_case(P, nh, L, d, torch.bfloat16, std, seed=L * 131 + d + int(std),
+                            prescaled=prescaled)
     assert np.all(np.isfinite(o))
     for j in range(nh):
         ref = O.attention(q[j], k[j], v[j])
@@ -100,18 +117,20 @@ def test_attention_bf16(P, L, d, std):
         assert e < 1e-2  # typical bf16 P rounding error is ~3e-3
 
 
+@pytest.mark.parametrize("prescaled", [False, True], ids=["plain-q", "prescaled-q"])
 @pytest.mark.parametrize("L", [1, 37, 128, 300])
 @pytest.mark.parametrize("d", [64, 128])
-def test_attention_f32(P, L, d):
+def test_attention_f32(P, L, d, prescaled):
     nh = 3
-    q, k, v, o = _attn_case(P, nh, L, d, torch.float32, 1.0, seed=L + d)
+    q, k, v, o = _attn_case(P, nh, L, d, torch.float32, 1.0, seed=L + d, prescaled=prescaled)
     for j in range(nh):
         assert rel_err(o[:, j * d:(j + 1) * d], O.attention(q[j], k[j], v[j])) < 1e-5
 
 
+@pytest.mark.parametrize("prescaled", [False, True], ids=["plain-q", "prescaled-q"])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("L", [300, 1000])
-def test_attention_growing_and_spiking_scores(P, d, L):
+def test_attention_growing_and_spiking_scores(P, d, L, prescaled):
     """Scores that grow along the key axis (the reference max must move on
     later tiles, by far more than the lazy bound) and one key whose score
     dwarfs all others (a probability that would overflow without a rescale)."""
@@ -127,7 +146,11 @@ def test_attention_growing_and_spiking_scores(P, d, L):
     vt = np.zeros((nh, d, vt_ld), np.float32)
     vt[:, :, :L] = v.transpose(0, 2, 1)
     o = torch.empty((L, nh * d), dtype=torch.bfloat16, device="cuda")
-    P.attention(to_dev(q, torch.bfloat16), to_dev(k, torch.bfloat16), to_dev(vt, torch.bfloat16), o)
+    q_dev = q
+    if prescaled:
+        q_dev, q = prescale_q(P, q, d, torch.bfloat16)
+    P.attention(to_dev(q_dev, torch.bfloat16), to_dev(k, torch.bfloat16), to_dev(vt, torch.bfloat16),
+                o, q_prescaled=prescaled)
     got = to_np(o)
     assert np.all(np.isfinite(got))
     for j in range(nh):
@@ -152,7 +175,7 @@ def test_attention_uniform_and_single_key(P):
 
 # -------------------------------------------------------------------- GEMM
 
-KINDS = ["bias", "gelu", "gate_residual", "qkv", "euler"]
+KINDS = ["bias", "gelu", "gate_residual", "qkv", "qkv_prescaled", "euler"]
 
 
 def _linear_case(P, kind, M, N, K, dtype, seed):
@@ -184,7 +207,7 @@ def _linear_case(P, kind, M, N, K, dtype, seed):
         v = torch.empty((M, N), device="cuda")
         P.linear(ad, wtd, P.ACID_EPI_EULER, bd, out=x, v_out=v, dsigma=-0.125)
         return [(to_np(v), y, 1e-5), (to_np(x) - x0, -0.125 * y, 1e-5)]
-    # qkv: N = 3 * heads * d
+    # qkv: N = 3 * heads * d; qkv_prescaled stores Q times log2(e)/sqrt(d)
     d = 64
     nh = N // (3 * d)
     H = nh * d
@@ -192,9 +215,10 @@ def _linear_case(P, kind, M, N, K, dtype, seed):
     q = torch.empty((nh, M, d), dtype=dtype, device="cuda")
     k = torch.empty((nh, M, d), dtype=dtype, device="cuda")
     vt = torch.zeros((nh, d, vt_ld), dtype=dtype, device="cuda")
-    P.linear(ad, wtd, P.ACID_EPI_QKV, bd, q=q, k=k, vt=vt, n_heads=nh, head_dim=d)
+    pre = kind == "qkv_prescaled"
+    P.linear(ad, wtd, P.ACID_EPI_QKV, bd, q=q, k=k, vt=vt, n_heads=nh, head_dim=d, q_prescale=pre)
     tol = 1e-5 if dtype == torch.float32 else 4e-3
-    yq = y[:, :H].reshape(M, nh, d).transpose(1, 0, 2)
+    yq = y[:, :H].reshape(M, nh, d).transpose(1, 0, 2) * (P.q_scale(d) if pre else 1.0)
     yk = y[:, H:2 * H].reshape(M, nh, d).transpose(1, 0, 2)
     yv = y[:, 2 * H:].reshape(M, nh, d).transpose(1, 2, 0)
     return [(to_np(q), yq, tol), (to_np(k), yk, tol), (to_np(vt)[:, :, :M], yv, tol)]
@@ -214,10 +238,33 @@ def test_linear_large_tiles_ragged(P, kind):
     """Large ragged shapes: ragged M over many 256-row tiles and, for
     N = 2176, a half-width last feature tile."""
     M, K = 8200, 256
-    N = 2304 if kind == "qkv" else 2176
+    N = 2304 if kind.startswith("qkv") else 2176
     # the qkv case in _linear_case uses d = 64: 2304 = 3 x 12 x 64
     for got, ref, tol in _linear_case(P, kind, M, N, K, torch.bfloat16, seed=17):
         assert rel_err(got, ref) < tol, kind
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_linear_qkv_prescale_fp32_bits(P, d):
+    """fp32 QKV with q_prescale: Q is the float32 product of the unscaled
+    Q with log2(e)/sqrt(d) bit for bit; K and V are unchanged."""
+    M, nh, K = 300, 2, 256
+    N = 3 * nh * d
+    rng = np.random.default_rng(d)
+    a = to_dev(rng.normal(size=(M, K)).astype(np.float32))
+    wt = to_dev((rng.normal(size=(N, K)) / math.sqrt(K)).astype(np.float32))
+    b = to_dev(rng.normal(size=N).astype(np.float32) * 0.1)
+    outs = []
+    for pre in (False, True):
+        q = torch.empty((nh, M, d), device="cuda")
+        k = torch.empty((nh, M, d), device="cuda")
+        vt = torch.zeros((nh, d, (M + 7) // 8 * 8), device="cuda")
+        P.linear(a, wt, P.ACID_EPI_QKV, b, q=q, k=k, vt=vt, n_heads=nh, head_dim=d, q_prescale=pre)
+        outs.append((to_np(q), to_np(k), to_np(vt)))
+    (q0, k0, v0), (q1, k1, v1) = outs
+    np.testing.assert_array_equal(q1, (q0 * np.float32(P.q_scale(d))).astype(np.float32))
+    np.testing.assert_array_equal(k1, k0)
+    np.testing.assert_array_equal(v1, v0)
 
 
 def test_linear_shape_errors(P):

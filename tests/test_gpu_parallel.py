@@ -33,9 +33,10 @@ def P():
     return need_gpu()
 
 
+@pytest.mark.parametrize("pre", [False, True], ids=["plain-q", "prescaled-q"])
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
 @pytest.mark.parametrize("M,nh,d,F", [(1, 2, 64, 128), (300, 2, 64, 384), (513, 4, 128, 640)])
-def test_linear_qkv_gelu(P, dtype, M, nh, d, F):
+def test_linear_qkv_gelu(P, dtype, M, nh, d, F, pre):
     H = nh * d
     N, K = 3 * H + F, 256
     rng = np.random.default_rng(M + F)
@@ -51,9 +52,10 @@ def test_linear_qkv_gelu(P, dtype, M, nh, d, F):
     vt = torch.zeros((nh, d, vt_ld), dtype=dtype, device="cuda")
     cat = torch.full((M, H + F), 7.0, dtype=dtype, device="cuda")  # attention half untouched
     P.linear(to_dev(a, dtype), to_dev(w.T.copy(), dtype), P.ACID_EPI_QKV_GELU, to_dev(b),
-             q=q, k=k, vt=vt, n_heads=nh, head_dim=d, out=cat[:, H:])
+             q=q, k=k, vt=vt, n_heads=nh, head_dim=d, out=cat[:, H:], q_prescale=pre)
     tol = 1e-5 if dtype == torch.float32 else 4e-3
-    assert rel_err(to_np(q), y[:, :H].reshape(M, nh, d).transpose(1, 0, 2)) < tol
+    qs = P.q_scale(d) if pre else 1.0
+    assert rel_err(to_np(q), y[:, :H].reshape(M, nh, d).transpose(1, 0, 2) * qs) < tol
     assert rel_err(to_np(k), y[:, H:2 * H].reshape(M, nh, d).transpose(1, 0, 2)) < tol
     assert rel_err(to_np(vt)[:, :, :M], y[:, 2 * H:3 * H].reshape(M, nh, d).transpose(1, 2, 0)) < tol
     assert rel_err(to_np(cat[:, H:]), O.gelu_tanh(y[:, 3 * H:])) < tol
