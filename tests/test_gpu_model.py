@@ -184,3 +184,34 @@ def test_denoise_loop_bf16_small(P):
     ok = ~np.isnan(otr["s"])
     np.testing.assert_allclose(tr["s"][ok], otr["s"][ok], rtol=2e-2)
     assert rel_err(to_np(x) - x0, xr - x0) < 2e-2
+
+
+def test_kernel_timer_counts_and_leaves_results_alone(P):
+    """The per-kernel event timer (the bench's per-class durations): a timed
+    loop gives the same bits as an untimed one, and counts one launch per
+    kernel of each class (per computed block: one of each GEMM and attention,
+    two LN-modulates; every step: drift, cache, head)."""
+    cfg = ai.SMALL
+    m, _ = make_model(P, cfg, max_steps=cfg.n_steps)
+    x0 = ai.latents(cfg)
+    sig = ai.sigmas(cfg.n_steps)
+    gate = dict(tau_low=0.05, tau_high=0.2, delta=0.01)
+    x_plain = to_dev(x0)
+    tr = m.denoise_loop(x_plain, sig, mode="acid", **gate)
+    m.reset_timing()
+    m.set_timing(True)
+    x_timed = to_dev(x0)
+    tr2 = m.denoise_loop(x_timed, sig, mode="acid", **gate)
+    torch.cuda.synchronize()
+    tim = m.timing()
+    m.set_timing(False)
+    assert torch.equal(x_plain, x_timed)
+    assert np.array_equal(tr["compute"], tr2["compute"])
+    n_comp = int(tr["compute"].sum())
+    blocks = n_comp * cfg.n_blocks
+    for name in ("attention", "gemm_qkv", "gemm_proj", "gemm_ffn1", "gemm_ffn2"):
+        assert tim[name][1] == blocks, (name, tim[name])
+        assert tim[name][0] > 0.0
+    assert tim["ln_mod"][1] == 2 * blocks + cfg.n_steps
+    assert tim["gemm_head"][1] == cfg.n_steps
+    assert tim["drift"][1] == cfg.n_steps
