@@ -22,7 +22,7 @@ from ._lib import (ACID_BF16, ACID_CACHE_APPLY, ACID_CACHE_STORE, ACID_EPI_BIAS,
                    TRACE_DTYPE, check, lib)
 
 __all__ = ["Model", "gate", "GateState", "gate_device_sequence", "cache_apply", "easycache_reuse", "attention", "linear",
-           "ln_modulate", "version", "AcidError", "KERNEL_CLASSES"]
+           "ln_modulate", "q_scale", "version", "AcidError", "KERNEL_CLASSES"]
 
 
 def _torch():

@@ -318,29 +318,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
     m_nx = m_run + d_nx;
     a_nx = __builtin_amdgcn_exp2f(-d_nx);
   };
-  // p = 2^(shifted score), rounded to bf16 as the B operand of the P V
-  // MFMAs; the row sum adds exactly those bf16 values (v_dot2 with (1, 1)).
-  auto probs = [&](const f32x16(&s)[2], bf16x8(&pf)[2][2], float& psum) {
-    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
-    float ps[2] = {0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        u32x4 w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 8 * k2 + 2 * e;
-          const bf16x2 pr = {(bf16)__builtin_amdgcn_exp2f(s[kb][r]),
-                             (bf16)__builtin_amdgcn_exp2f(s[kb][r + 1])};
-          ps[e & 1] = __builtin_amdgcn_fdot2_f32_bf16(pr, one, ps[e & 1], false);
-          w[e] = __builtin_bit_cast(uint32_t, pr);
-        }
-        pf[kb][k2] = __builtin_bit_cast(bf16x8, w);
-      }
-    psum = ps[0] + ps[1];
-  };
-  // The same for the 16 keys of one P V K-step (kb, k2) only, adding into ps.
+  // p = 2^(shifted score) for the 16 keys of one P V K-step (kb, k2), rounded
+  // to bf16 as the B operand of the P V MFMAs; the row sum adds exactly those
+  // bf16 values (v_dot2 with (1, 1)) into ps.
   auto probs_part = [&](const f32x16(&s)[2], int kb, int k2, bf16x8(&pf)[2][2],
                         float(&ps)[2]) {
     const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
@@ -354,6 +334,15 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
       w[e] = __builtin_bit_cast(uint32_t, pr);
     }
     pf[kb][k2] = __builtin_bit_cast(bf16x8, w);
+  };
+  // The whole tile.
+  auto probs = [&](const f32x16(&s)[2], bf16x8(&pf)[2][2], float& psum) {
+    float ps[2] = {0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) probs_part(s, kb, k2, pf, ps);
+    psum = ps[0] + ps[1];
   };
   // O^T (d x queries) += V^T P^T.  Contraction slot (lg, e) of K-step
   // (kb, k2) is S^T row kb*32 + 16 k2 + 8 (e/4) + 4 lg + e%4, i.e. key
