@@ -5,7 +5,9 @@
 //   Macro tile 256 (tokens) x 256 (features), K in steps of 64, 8 waves in a
 //   2 x 4 grid (two per SIMD), each wave 128 x 64 = 4 x 2 MFMA blocks of
 //   32 x 32.  Operands go global -> LDS directly (global_load_lds_dwordx4,
-//   no staging registers) into two 64 KB stages, K-contiguous 128-byte rows
+//   no staging registers) into a ring of 32 KB operand tiles (three for
+//   the activations, fetched two K-steps ahead, two for the weights, one
+//   ahead: 160 KB, the whole LDS), K-contiguous 128-byte rows
 //   (whole cache lines, so the L2 request rate stays within budget) with an
 //   XOR swizzle that is conflict-free for gfx950's 64 LDS banks.  One
 //   barrier per K-step, placed before the last 16-wide sub-step so the
@@ -251,10 +253,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
                                                                    int64_t M, int N, int K,
                                                                    Epi e) {
   if (e.pred && *e.pred == 0) return;
-  // Two stages of A and B tiles, one LDS object per tile so the compiler can
-  // tell the stage being read from the stage being filled.
+  // Three A tiles and two B tiles, one LDS object per tile so the compiler
+  // can tell the tile being read from the tile being filled.
   __shared__ __attribute__((aligned(1024))) bf16 As0[kTileElems], Bs0[kTileElems];
   __shared__ __attribute__((aligned(1024))) bf16 As1[kTileElems], Bs1[kTileElems];
+  __shared__ __attribute__((aligned(1024))) bf16 As2[kTileElems];
 
   const int tiles_n = (N + BN - 1) / BN;
   const int64_t tiles_m = (M + BM - 1) / BM;
@@ -335,10 +338,11 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
 #pragma unroll
     for (int i = 0; i < 4; ++i) dma16(b_base, b_off[i] + k0 * 2, lb + i * 1024);
   };
-  // The last K-step of a stage with the refill of its buffer interleaved:
-  // one DMA after each of the 8 MFMAs (order pinned by scheduling barriers).
+  // The last K-step of a stage with the refill of its tiles interleaved: one
+  // DMA after each of the 8 MFMAs (order pinned by scheduling barriers), the
+  // weight tile (K offset kb) first, the activation tile (ka) last.
   auto mma_refill = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2], const bf16* As,
-                        const bf16* Bs, int kn) {
+                        const bf16* Bs, int ka, int kb) {
     const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
     const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
 #pragma unroll
@@ -348,27 +352,35 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
         const int j = mb * 2 + nb, i = j & 3;
         if (j < 4)
-          dma16(a_base, a_off[i] + kn * 2, la + i * 1024);
+          dma16(b_base, b_off[i] + kb * 2, lb + i * 1024);
         else
-          dma16(b_base, b_off[i] + kn * 2, lb + i * 1024);
+          dma16(a_base, a_off[i] + ka * 2, la + i * 1024);
         __builtin_amdgcn_sched_barrier(0);
       }
   };
+  auto load_a = [&](const bf16* As, int k0) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(a_base, a_off[i] + k0 * 2, la + i * 1024);
+  };
 
   const int KT = K / BK;  // even: K % 128 == 0
-  // Prologue: stages 0 and 1 in flight, stage 0 landed, first fragments read.
+  auto kc = [&](int k) { return (k < KT ? k : KT - 1) * BK; };
+  // Three A stages and two B stages (160 KB): the activations, streamed from
+  // HBM, are fetched two stages ahead, the weights one.  Prologue: A 0, B 0,
+  // A 1, B 1, A 2 in flight; stage 0 landed (vmcnt 12).
   load_stage(As0, Bs0, 0);
-  load_stage(As1, Bs1, BK);
-  __builtin_amdgcn_s_waitcnt((8 & 15) | (7 << 4) | (15 << 8));  // vmcnt(8): stage 0 landed
+  load_stage(As1, Bs1, kc(1));
+  load_a(As2, kc(2));
+  __builtin_amdgcn_s_waitcnt((12 & 15) | (7 << 4) | (15 << 8));
   __builtin_amdgcn_s_barrier();
   read_frags(As0, Bs0, sl[0], fa0, fb0);
 
-  // Stage kt (buffer kt % 2): K-steps 0..2 with the next step's fragments
-  // read behind each MFMA group; then this wave's reads of the buffer are
-  // done and stage kt+1 has landed (wait), barrier (everyone's are), read
-  // stage kt+1's first fragments and run K-step 3 with the refill of this
-  // buffer (stage kt+2) interleaved.  Past the last stage the refill reloads
-  // stage KT-1 into a buffer that is never read again.
+  // Stage kt reads A[kt % 3], B[kt % 2]; in its last K-step it refills
+  // B[kt % 2] with stage kt + 2 and then A[kt % 3] with stage kt + 3.  At
+  // its barrier the group issued last (A of stage kt + 2) may still be in
+  // flight: vmcnt(4).
+  int kt = 0;
 #define GEMM_STAGE(AS, BS, AN, BN_)                                              \
   {                                                                            \
     read_frags(AS, BS, sl[1], fa1, fb1);                                       \
@@ -383,18 +395,29 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
     __builtin_amdgcn_sched_barrier(0);                                         \
     mma(fa0, fb0);                                                             \
     __builtin_amdgcn_sched_barrier(0);                                         \
-    wait_all();                                                                \
+    __builtin_amdgcn_s_waitcnt(4 | (7 << 4) | (0 << 8));                       \
     __builtin_amdgcn_s_barrier();                                              \
     read_frags(AN, BN_, sl[0], fa0, fb0);                                      \
     __builtin_amdgcn_sched_barrier(0);                                         \
-    mma_refill(fa1, fb1, AS, BS, (kt + 2 < KT ? kt + 2 : KT - 1) * BK);        \
+    mma_refill(fa1, fb1, AS, BS, kc(kt + 3), kc(kt + 2));                      \
     __builtin_amdgcn_sched_barrier(0);                                         \
+    ++kt;                                                                      \
   }
-  for (int kt = 0; kt < KT; kt += 2) {
+  while (kt + 6 <= KT) {
     GEMM_STAGE(As0, Bs0, As1, Bs1)
-    ++kt;
-    GEMM_STAGE(As1, Bs1, As0, Bs0)
-    --kt;
+    GEMM_STAGE(As1, Bs1, As2, Bs0)
+    GEMM_STAGE(As2, Bs0, As0, Bs1)
+    GEMM_STAGE(As0, Bs1, As1, Bs0)
+    GEMM_STAGE(As1, Bs0, As2, Bs1)
+    GEMM_STAGE(As2, Bs1, As0, Bs0)
+  }
+  if (kt + 2 <= KT) {
+    GEMM_STAGE(As0, Bs0, As1, Bs1)
+    GEMM_STAGE(As1, Bs1, As2, Bs0)
+  }
+  if (kt + 2 <= KT) {
+    GEMM_STAGE(As2, Bs0, As0, Bs1)
+    GEMM_STAGE(As0, Bs1, As1, Bs0)
   }
 #undef GEMM_STAGE
   wait_all();  // the last refill lands before the workgroup's LDS is released
