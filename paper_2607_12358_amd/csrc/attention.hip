@@ -381,17 +381,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   // and forms the probabilities again.
   constexpr bool kOptimistic = D == 64;
   auto iter = [&](f32x16(&sc)[2], f32x16(&sn)[2], int it) {
-    // Staging of K_{it+2} and V_{it+1}, issued between the score MFMAs and
-    // the P V MFMAs (their buffers were last read in the previous
-    // iteration).  Issued there rather than at the top of the iteration,
-    // where all waves leave the barrier together, it costs 7% less time at
-    // d = 128.
-    auto stage_next = [&]() {
-      __builtin_amdgcn_sched_barrier(0);
-      if (it + 2 < nkv) stage_k_dma(it & 1, (it + 2 - has_tail) * BKV);
-      if (it + 1 < nkv) stage_v_dma((it + 1) & 1, (it + 1 - has_tail) * BKV);
-      __builtin_amdgcn_sched_barrier(0);
-    };
+    if (it + 2 < nkv) stage_k_dma(it & 1, (it + 2 - has_tail) * BKV);
+    if (it + 1 < nkv) stage_v_dma((it + 1) & 1, (it + 1 - has_tail) * BKV);
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (!kOptimistic) {
       m_run = m_nx;
       if (__any(g_nx)) {
@@ -419,6 +411,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
       probs_part(sc, 0, 0, pf, ps);
       probs_part(sc, 0, 1, pf, ps);
       scores(sn, (it + 1) & 1);
+      probs_part(sc, 1, 0, pf, ps);
+      probs_part(sc, 1, 1, pf, ps);
+      psum = ps[0] + ps[1];
+      l_run += psum;
+      pv(pf, it & 1);
+      row_max_check(sn);
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
       for (int i = 0; i < 2 * NK; ++i) {
@@ -427,14 +425,6 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         __builtin_amdgcn_sched_group_barrier(0x400, (16 + 2 * NK - 1) / (2 * NK), 0);
         __builtin_amdgcn_sched_group_barrier(0x002, (16 + 2 * NK - 1) / (2 * NK), 0);
       }
-      stage_next();
-      probs_part(sc, 1, 0, pf, ps);
-      probs_part(sc, 1, 1, pf, ps);
-      psum = ps[0] + ps[1];
-      l_run += psum;
-      pv(pf, it & 1);
-      row_max_check(sn);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
       for (int i = 0; i < 2 * ND; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -448,9 +438,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, (24 + 2 * ND - 1) / (2 * ND), 0);
       }
-    } else if constexpr (kOptimistic) {
-      probs(sc, pf, psum);
-      scores(sn, (it + 1) & 1);
+    } else {
+    probs(sc, pf, psum);
+    scores(sn, (it + 1) & 1);
+    if constexpr (kOptimistic) {
       // Each score MFMA with one fragment read and a share of the
       // exponentials.
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
@@ -460,7 +451,7 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, (66 + 2 * NK - 1) / (2 * NK), 0);
       }
-      stage_next();
+      __builtin_amdgcn_sched_barrier(0);
       if (__any(!(psum <= 256.0f))) {
         float mx = sc[0][0];
 #pragma unroll
@@ -497,12 +488,12 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         }
       }
     } else {
-      // Plain Q, d = 128: four fragment reads ahead, then each score MFMA
-      // with one more read and a share of the exponentials; then each P V
-      // MFMA with one read and a share of the row max and shift of the next
-      // tile.
-      probs(sc, pf, psum);
-      scores(sn, (it + 1) & 1);
+      l_run += psum;
+      pv(pf, it & 1);
+      row_max_shift(sn);
+      // Four fragment reads ahead, then each score MFMA with one more read
+      // and a share of the exponentials, then each P V MFMA with one read
+      // and a share of the row max and shift of the next tile.
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
       for (int i = 0; i < 2 * NK; ++i) {
@@ -510,17 +501,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, (66 + 2 * NK - 1) / (2 * NK), 0);
       }
-      stage_next();
-      l_run += psum;
-      pv(pf, it & 1);
-      row_max_shift(sn);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
       for (int i = 0; i < 4 * ND; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, (56 + 4 * ND - 1) / (4 * ND), 0);
       }
+    }
     }
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);  // this iteration's staging has landed
