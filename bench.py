@@ -238,7 +238,7 @@ def run_sweep(args, m, cfg, x0, text_d, sig, mode: str = "acid") -> int:
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3, help="timed denoise loops")
+    ap.add_argument("--steps", type=int, default=5, help="timed denoise loops")
     ap.add_argument("--warmup", type=int, default=1, help="untimed denoise loops")
     ap.add_argument("--workload", default="wan2.1-1.3b-shape")
     ap.add_argument("--n-steps", type=int, default=None, help="denoising steps per loop")
