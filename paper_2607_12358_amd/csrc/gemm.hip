@@ -277,6 +277,8 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
 
   // Load-side addressing: byte offsets from the tile's first row (rows past
   // the edge are clamped; they only feed outputs that are never stored).
+  // The K offset of a stage is added to the scalar base, so the per-lane
+  // offsets stay fixed and a DMA needs no vector arithmetic.
   const int chunk_even = (lane & 7) ^ (lane >> 4);
   const int chunk_odd = (lane & 7) ^ ((lane >> 4) ^ 4);
   const uint64_t a_base = uniform_ptr(A + m0 * K);
@@ -334,9 +336,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
     const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
     const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(a_base, a_off[i] + k0 * 2, la + i * 1024);
+    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(b_base, b_off[i] + k0 * 2, lb + i * 1024);
+    for (int i = 0; i < 4; ++i) dma16(b_base + (uint32_t)(k0 * 2), b_off[i], lb + i * 1024);
   };
   // The last K-step of a stage with the refill of its tiles interleaved: one
   // DMA after each of the 8 MFMAs (order pinned by scheduling barriers), the
@@ -345,6 +347,7 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
                         const bf16* Bs, int ka, int kb) {
     const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
     const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
+    const uint64_t ak = a_base + (uint32_t)(ka * 2), bk = b_base + (uint32_t)(kb * 2);
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -352,16 +355,16 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
         const int j = mb * 2 + nb, i = j & 3;
         if (j < 4)
-          dma16(b_base, b_off[i] + kb * 2, lb + i * 1024);
+          dma16(bk, b_off[i], lb + i * 1024);
         else
-          dma16(a_base, a_off[i] + ka * 2, la + i * 1024);
+          dma16(ak, a_off[i], la + i * 1024);
         __builtin_amdgcn_sched_barrier(0);
       }
   };
   auto load_a = [&](const bf16* As, int k0) {
     const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(a_base, a_off[i] + k0 * 2, la + i * 1024);
+    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
   };
 
   const int KT = K / BK;  // even: K % 128 == 0
