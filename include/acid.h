@@ -91,7 +91,8 @@ typedef enum { ACID_BLOCK_SEQUENTIAL = 0, ACID_BLOCK_PARALLEL = 1 } acid_block_k
 /* Shape of the DiT stack.  Token rows are ordered text first, then video.
  * hidden = n_heads * head_dim.  Supported: head_dim 64 or 128; hidden
  * (<= 4096) and ffn multiples of 128 (every GEMM's N and K); freq_dim even
- * and <= 1024. */
+ * and <= 1024; L = n_text + n_video within acid_attention's and
+ * acid_linear's size limits (ACID_ERR_SHAPE otherwise). */
 typedef struct {
   int32_t n_blocks;
   int32_t hidden;
@@ -355,7 +356,9 @@ acid_status acid_ln_modulate(int32_t out_dtype, const float* x_dev,
  * log2(e)/sqrt(d) (the float value 1.4426950408889634f / sqrtf(d)) and
  * rounded to `dtype`, as the QKV epilogue writes it with q_prescale set
  * (the softmax then needs no per-score scaling); other values:
- * ACID_ERR_INVALID_ARG. */
+ * ACID_ERR_INVALID_ARG.  Size limits (ACID_ERR_SHAPE beyond them):
+ * seq_len * n_heads < 2^26, and for bf16 head_dim * vt_ld * 2 < 2^31
+ * (32-bit per-head offsets). */
 acid_status acid_attention(int32_t dtype, int32_t n_heads, int64_t seq_len,
                            int32_t head_dim, const void* q_dev,
                            const void* k_dev, const void* vt_dev,
@@ -396,7 +399,8 @@ typedef struct {
 } acid_epilogue_args;
 
 /* Fused GEMM: a [M][K] and wt = W transposed [N][K], both in `dtype`;
- * N % 128 == 0, K % 128 == 0, any M >= 0 (ACID_ERR_SHAPE otherwise). */
+ * N % 128 == 0, K % 128 == 0, N and K <= 2^22, 0 <= M <= 2^30 with
+ * ceil(M / 256) * ceil(N / 256) < 2^23 (ACID_ERR_SHAPE otherwise). */
 acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K,
                         const void* a_dev, const void* wt_dev,
                         const acid_epilogue_args* epi, hipStream_t stream);

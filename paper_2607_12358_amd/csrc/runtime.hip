@@ -36,6 +36,28 @@ inline size_t align_up(size_t a) { return (a + kAlign - 1) / kAlign * kAlign; }
 
 int esize(int dtype) { return dtype == ACID_BF16 ? 2 : 4; }
 
+// Size limits of the kernels' index arithmetic: the bf16 attention kernel
+// addresses a head's K and V^T with 32-bit offsets, the bf16 GEMM a tile's
+// operand rows with 32-bit offsets (256 rows of K elements), and a launch
+// holds fewer than 2^32 work-items per grid dimension.
+acid_status check_attention_size(int dtype, int n_heads, int64_t L, int d, int64_t vt_ld) {
+  const int64_t lim = 0x7fffffff;
+  if (dtype == ACID_BF16 && vt_ld > lim / (2 * d))
+    return set_error(ACID_ERR_SHAPE, "bf16 attention: head_dim * vt_ld * 2 bytes must be < 2^31");
+  if (L > lim / 32 || L * n_heads > lim / 32)  // the fp32 kernel: 64 work-items per query
+    return set_error(ACID_ERR_SHAPE, "attention: seq_len %lld x n_heads %d exceeds the grid limit",
+                     (long long)L, n_heads);
+  return ACID_OK;
+}
+acid_status check_linear_size(int64_t M, int N, int K) {
+  if (K > (1 << 22) || N > (1 << 22))
+    return set_error(ACID_ERR_SHAPE, "linear: N %d and K %d must be <= 2^22", N, K);
+  if (M > (int64_t)1 << 30 || (M + 255) / 256 * ((N + 255) / 256) >= (1 << 23))
+    return set_error(ACID_ERR_SHAPE, "linear: M %lld x N %d exceeds the grid limit", (long long)M,
+                     N);
+  return ACID_OK;
+}
+
 acid_status check_config(const acid_dit_config* c) {
   if (!c) return set_error(ACID_ERR_INVALID_ARG, "config is NULL");
   if (c->dtype != ACID_F32 && c->dtype != ACID_BF16)
@@ -56,7 +78,14 @@ acid_status check_config(const acid_dit_config* c) {
   if (c->block_kind != ACID_BLOCK_SEQUENTIAL && c->block_kind != ACID_BLOCK_PARALLEL)
     return set_error(ACID_ERR_INVALID_ARG, "block_kind %d is not SEQUENTIAL or PARALLEL",
                      c->block_kind);
-  return ACID_OK;
+  // Every attention and GEMM of the step within the kernels' size limits:
+  // L tokens, N up to 3H + F (the parallel block's fused projection), K up
+  // to H + F.
+  const int64_t L = (int64_t)c->n_video + c->n_text;
+  ACID_TRY(check_attention_size(c->dtype, c->n_heads, L, c->head_dim, round_up(L, 8)));
+  if ((int64_t)3 * c->hidden + c->ffn > (1 << 22))
+    return set_error(ACID_ERR_SHAPE, "3 * hidden + ffn must be <= 2^22");
+  return check_linear_size(L, 3 * c->hidden + c->ffn, c->hidden + c->ffn);
 }
 
 // ------------------------------------------------------------ arena layout
@@ -1033,6 +1062,7 @@ acid_status acid_attention(int32_t dtype, int32_t n_heads, int64_t seq_len, int3
   if (vt_ld < round_up(seq_len, 8) || vt_ld % 8)
     return set_error(ACID_ERR_SHAPE, "vt_ld %lld must be a multiple of 8 and >= round_up(L, 8)",
                      (long long)vt_ld);
+  ACID_TRY(check_attention_size(dtype, n_heads, seq_len, head_dim, vt_ld));
   if (seq_len > 0 && (!q_dev || !k_dev || !vt_dev || !o_dev))
     return set_error(ACID_ERR_INVALID_ARG, "NULL argument");
   hipError_t e = launch_attention(dtype, n_heads, seq_len, head_dim, q_dev, k_dev, vt_dev, vt_ld,
@@ -1050,6 +1080,7 @@ acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K, const vo
   if (M < 0 || N <= 0 || K <= 0) return set_error(ACID_ERR_INVALID_ARG, "bad M/N/K");
   if (N % 128 || K % 128)
     return set_error(ACID_ERR_SHAPE, "N %d and K %d must be multiples of 128", N, K);
+  ACID_TRY(check_linear_size(M, N, K));
   if (M == 0) return ACID_OK;
   if (!a_dev || !wt_dev || !epi->bias) return set_error(ACID_ERR_INVALID_ARG, "NULL operand or bias");
   switch (epi->kind) {

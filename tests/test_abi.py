@@ -51,7 +51,8 @@ def test_workload_configs_accepted_and_manifest_matches(lib, cfg):
 @pytest.mark.parametrize("field,value,status", [
     ("head_dim", 96, L.ACID_ERR_SHAPE), ("hidden", 1000, L.ACID_ERR_SHAPE),
     ("ffn", 1000, L.ACID_ERR_SHAPE), ("n_blocks", 0, L.ACID_ERR_INVALID_ARG),
-    ("freq_dim", 7, L.ACID_ERR_SHAPE), ("dtype", 5, L.ACID_ERR_INVALID_ARG)])
+    ("freq_dim", 7, L.ACID_ERR_SHAPE), ("dtype", 5, L.ACID_ERR_INVALID_ARG),
+    ("n_video", 1 << 26, L.ACID_ERR_SHAPE), ("ffn", 1 << 22, L.ACID_ERR_SHAPE)])
 def test_config_errors(lib, field, value, status):
     c = L.config_c(ai.TINY)
     setattr(c, field, value)
@@ -80,6 +81,25 @@ def test_prescaled_q_flags_checked(lib):
                            None) == L.ACID_ERR_INVALID_ARG
     e.q_prescale = 1
     assert lib.acid_linear(L.ACID_BF16, 0, 384, 128, None, None, C.byref(e), None) == 0
+
+
+def test_kernel_size_limits_checked(lib):
+    """Sizes beyond the kernels' 32-bit offsets and grid limits are refused
+    before any GPU work (the pointers are never looked at)."""
+    def attn(dtype, nh, L_, d):
+        ld = (L_ + 7) // 8 * 8
+        return lib.acid_attention(dtype, nh, L_, d, None, None, None, ld, None, 0, None)
+    assert attn(L.ACID_BF16, 1, 9_000_000, 128) == L.ACID_ERR_SHAPE    # 2 d vt_ld >= 2^31
+    assert attn(L.ACID_BF16, 1, 9_000_000, 64) == L.ACID_ERR_INVALID_ARG  # within: NULL check
+    assert attn(L.ACID_F32, 64, 2_000_000, 64) == L.ACID_ERR_SHAPE     # L n_heads >= 2^26
+    assert attn(L.ACID_F32, 32, 2_000_000, 64) == L.ACID_ERR_INVALID_ARG
+    e = L.EpilogueArgsC()
+    e.kind = L.ACID_EPI_BIAS
+    for M, N, K, st in [(1 << 20, 1 << 23, 128, L.ACID_ERR_SHAPE), (8, 128, 1 << 23, L.ACID_ERR_SHAPE),
+                        ((1 << 30) + 1, 128, 128, L.ACID_ERR_SHAPE),
+                        (1 << 24, 1 << 17, 128, L.ACID_ERR_SHAPE),
+                        (1 << 22, 1 << 16, 128, L.ACID_ERR_INVALID_ARG)]:
+        assert lib.acid_linear(L.ACID_BF16, M, N, K, None, None, C.byref(e), None) == st, (M, N, K)
 
 
 def test_device_gate_and_graph_loop_argument_errors(lib):
