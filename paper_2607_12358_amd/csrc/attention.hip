@@ -26,6 +26,8 @@
 //   that the P V product uses.
 // fp32 path: one wave per (head, query), online softmax in fp32 (for the
 //   fp32 configuration).
+#include <atomic>
+
 #include "common.h"
 
 namespace acid {
@@ -394,7 +396,10 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
           for (int r = 0; r < 16; ++r) o[db][r] *= a_nx;
         if constexpr (kPre) {
           sub_all(sc, d_nx);
-          set_cneg(-m_run);
+          // -m_run in place: (-m) - d equals -(m + d) exactly, and updating
+          // cneg's own registers spares the common path a 16-register copy.
+#pragma unroll
+          for (int r = 0; r < 16; ++r) cneg[r] -= d_nx;
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -652,13 +657,17 @@ hipError_t launch_bf16(int n_heads, int64_t L, const void* q, const void* k, con
                        const int32_t* pred) {
   constexpr int NW = D == 128 ? 8 : 4;
   constexpr int BQ = 32 * NW;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t err = hipFuncSetAttribute((const void*)attn_bf16_kernel<D, NW, kPre>,
-                                         hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         (int)AttnLds<D>::BYTES);
+  // The dynamic-LDS attribute is set once per device (one bit each).
+  static std::atomic<uint64_t> attr_set{0};
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
+  if (!(attr_set.load(std::memory_order_acquire) & bit)) {
+    err = hipFuncSetAttribute((const void*)attn_bf16_kernel<D, NW, kPre>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)AttnLds<D>::BYTES);
     if (err != hipSuccess) return err;
-    attr_set = true;
+    attr_set.fetch_or(bit, std::memory_order_release);
   }
   const float scale_log2 = attn_q_scale(D);
   dim3 grid((unsigned)(((L + BQ - 1) / BQ) * n_heads));
