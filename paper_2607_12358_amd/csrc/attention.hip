@@ -531,6 +531,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   __syncthreads();
   if constexpr (kPre) set_cneg(0.0f);
   scores(sa, 0);
+  // Every wave has read K tile 0 before the first iteration restages its
+  // buffer (a wave running ahead would otherwise overwrite it).
+  __syncthreads();
   if (has_tail) {
     // Keys past L get score -inf.  S^T row kb*32 + 8 (r/4) + 4 lg + r%4
     // holds key j0 + key_perm(row).
