@@ -184,9 +184,22 @@ def parse_list(text: str):
     return [float(v) for v in text.split(",") if v]
 
 
-def run_sweep(args, m, cfg, x0, text_d, sig, mode: str = "acid") -> int:
-    """No-cache, fixed-threshold and ACID runs on one workload: computed
-    steps, PSNR of x_N against the no-cache x_N, seconds per loop."""
+def sweep_grid(taus: str, pairs: str, deltas: str, delta_fixed: float):
+    """(kind, tau_low, tau_high, delta) points: fixed thresholds, then each
+    ACID pair with each delta."""
+    grid = [("fixed", t, t, delta_fixed) for t in parse_list(taus)]
+    for pair in pairs.split(","):
+        lo, hi = (float(v) for v in pair.split(":"))
+        grid += [("acid", lo, hi, d) for d in parse_list(deltas)]
+    return grid
+
+
+def sweep(m, cfg, x0, text_d, sig, grid, mode: str = "acid", warmup: int = 0, steps: int = 1,
+          outputs=None):
+    """No-cache, then each grid point: computed steps, PSNR of x_N against the
+    no-cache x_N, seconds per loop (median of `steps` timed loops after
+    `warmup`).  Each run dict carries its trace; with `outputs` (a list) the
+    x_N of every run (no-cache first) is appended to it."""
     import statistics
 
     import torch
@@ -195,26 +208,26 @@ def run_sweep(args, m, cfg, x0, text_d, sig, mode: str = "acid") -> int:
 
     def timed(mode, **gate):
         times, tr = [], None
-        for k in range(args.warmup + args.steps):
+        for k in range(warmup + steps):
             x.copy_(x0)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             tr = m.denoise_loop(x, sig, text_d, mode=mode, **gate)
             torch.cuda.synchronize()
-            if k >= args.warmup:
+            if k >= warmup:
                 times.append(time.perf_counter() - t0)
         return statistics.median(times), tr
 
-    t_ref, _ = timed("nocache")
+    t_ref, tr_ref = timed("nocache")
     ref = x.clone()
+    if outputs is not None:
+        outputs.append(ref)
     runs = [{"mode": "nocache", "computed_steps": cfg.n_steps, "s_per_loop": t_ref,
-             "psnr_db": math.inf}]
-    grid = [("fixed", t, t, args.sweep_deltas_fixed) for t in parse_list(args.sweep_taus)]
-    for pair in args.sweep_pairs.split(","):
-        lo, hi = (float(v) for v in pair.split(":"))
-        grid += [("acid", lo, hi, d) for d in parse_list(args.sweep_deltas)]
+             "psnr_db": math.inf, "trace": tr_ref}]
     for kind, lo, hi, delta in grid:
         t, tr = timed(mode, tau_low=lo, tau_high=hi, delta=delta)
+        if outputs is not None:
+            outputs.append(x.clone())
         n_comp = int(tr["compute"].sum())
         sv = [float(v) for v in tr["s"] if math.isfinite(v)]
         ds = [abs(a - b) for a, b in zip(sv[1:], sv[:-1])]
@@ -222,13 +235,25 @@ def run_sweep(args, m, cfg, x0, text_d, sig, mode: str = "acid") -> int:
                "computed_steps": n_comp, "s_per_loop": t, "speedup_vs_nocache": t_ref / t,
                "psnr_db": psnr(x, ref),
                "steps_tau_high": int(sum(1 for v in tr["tau_used"][1:] if v == hi)),
+               "steps_tau_low": int(sum(1 for v in tr["tau_used"][1:] if v == lo)),
                "drift_s_min_max": [min(sv), max(sv)] if sv else None,
                "drift_step_change_median_max": ([float(sorted(ds)[len(ds) // 2]), float(max(ds))]
                                                 if ds else None),
-               "schedule": "".join("C" if c else "S" for c in tr["compute"])}
+               "schedule": "".join("C" if c else "S" for c in tr["compute"]),
+               "trace": tr}
         runs.append(run)
         log(f"{kind} tau=({lo}, {hi}) delta={delta}: {n_comp}/{cfg.n_steps} computed, "
             f"{t * 1e3:.2f} ms/loop, PSNR {run['psnr_db']:.2f} dB")
+    return runs
+
+
+def run_sweep(args, m, cfg, x0, text_d, sig, mode: str = "acid") -> int:
+    """The gate sweep of one workload as one JSON line (no traces)."""
+    grid = sweep_grid(args.sweep_taus, args.sweep_pairs, args.sweep_deltas,
+                      args.sweep_deltas_fixed)
+    runs = sweep(m, cfg, x0, text_d, sig, grid, mode, args.warmup, args.steps)
+    for r in runs:
+        del r["trace"]
     print(json.dumps({"sweep": {"workload": cfg.name, "signal": args.signal,
                                 "denoise_steps": cfg.n_steps,
                                 "loops_timed": args.steps, "runs": runs}}), flush=True)

@@ -203,6 +203,18 @@ acid_status acid_model_load_tensor(acid_model* m, int32_t id,
                                    const float* src_dev, int64_t n,
                                    hipStream_t stream);
 
+/* The same conversion from a host source (the form Algorithm 1's inputs
+ * suggest: the caller holds f_theta's parameters in host memory).  src_host
+ * is fp32 [in][out] (any host memory; n elements as above).  GEMM weights
+ * are staged through the model's workspace in whole source rows (its
+ * residual-stream buffer, whose contents are lost) and transposed on the
+ * device; other tensors are copied as they are.  Synchronises the stream:
+ * src_host may be freed or reused when the call returns.  Errors as
+ * acid_model_load_tensor. */
+acid_status acid_model_load_tensor_host(acid_model* m, int32_t id,
+                                        const float* src_host, int64_t n,
+                                        hipStream_t stream);
+
 /* Frees the host struct only (never device memory). */
 void acid_model_destroy(acid_model* m);
 
@@ -365,6 +377,12 @@ acid_status acid_attention(int32_t dtype, int32_t n_heads, int64_t seq_len,
                            int64_t vt_ld, void* o_dev, int32_t q_prescaled,
                            hipStream_t stream);
 
+/* The fp32 factor log2(e)/sqrt(head_dim) that a pre-scaled Q carries (see
+ * acid_attention's q_prescaled and the QKV epilogues' q_prescale): a caller
+ * that stores Q in that form multiplies by exactly this value before the one
+ * rounding to the operand dtype.  0 for head_dim <= 0. */
+float acid_q_scale(int32_t head_dim);
+
 /* Epilogues of the fused GEMM y = a W + b (acc in fp32). */
 typedef enum {
   ACID_EPI_BIAS = 0,          /* out fp32 [M][N] = y */
@@ -388,8 +406,8 @@ typedef struct {
   float* v_out;         /* EULER only, may be NULL */
   void* q;              /* QKV: [n_heads][M][head_dim] */
   void* k;              /* QKV: [n_heads][M][head_dim] */
-  void* vt;             /* QKV: [n_heads][head_dim][vt_ld] */
-  int64_t vt_ld;        /* QKV: >= round_up(M, 8) */
+  void* vt;             /* QKV: [n_heads][head_dim][vt_ld], 16-byte aligned */
+  int64_t vt_ld;        /* QKV: >= M, a multiple of 8 */
   int32_t n_heads;      /* QKV: N == 3 * n_heads * head_dim (QKV_GELU: >) */
   int32_t head_dim;     /* QKV */
   float dsigma;         /* EULER */

@@ -342,17 +342,20 @@ class AcidGate:
         i = self.step
         self.step += 1
         if i < p.n_warmup:
-            # Warmup: run the full model; accumulator and s_prev untouched.
+            # The base method's leading steps always run the model; the gate
+            # state is left as it was.
             return True, math.nan
         self.sigma_sum = self.sigma_sum + s_t
-        if self.s_prev is not None and abs(s_t - self.s_prev) <= p.delta:
-            tau = p.tau_high          # stable phase: cache aggressively
-        else:
-            tau = p.tau_low           # dynamic phase: cache conservatively
-        if self.sigma_sum <= tau:
-            compute = False           # reuse the cached residual
-        else:
-            compute = True            # run the model and reset
+        # A signal that moved by at most delta since the previous step
+        # selects the larger threshold (more skipping); any larger move, or
+        # no previous signal, selects the smaller one.
+        moved_little = self.s_prev is not None and abs(s_t - self.s_prev) <= p.delta
+        tau = p.tau_high if moved_little else p.tau_low
+        # Skip while the accumulated drift has not passed the threshold; a
+        # computed step starts the accumulation afresh.  (A NaN sum fails the
+        # comparison and so computes.)
+        compute = not (self.sigma_sum <= tau)
+        if compute:
             self.sigma_sum = 0.0
         self.s_prev = s_t
         return compute, tau

@@ -135,9 +135,9 @@ def attention(q, k, vt, o, stream=None, q_prescaled: bool = False) -> None:
 
 
 def q_scale(d: int) -> float:
-    """The float32 factor log2(e)/sqrt(d) a pre-scaled Q carries."""
-    import numpy as np
-    return float(np.float32(np.float32(1.4426950408889634) / np.sqrt(np.float32(d))))
+    """The float32 factor log2(e)/sqrt(d) a pre-scaled Q carries (the
+    library's own constant, acid_q_scale)."""
+    return float(lib().acid_q_scale(int(d)))
 
 
 def linear(a, wt, kind: int, bias, gate=None, out=None, v_out=None, q=None, k=None, vt=None,
@@ -213,6 +213,13 @@ class Model:
     def load_tensor(self, tid: int, src, stream=None) -> None:
         """src: fp32 device tensor of the manifest shape [in, out]."""
         check(lib().acid_model_load_tensor(self.h, tid, _ptr(src), src.numel(), _stream(stream)))
+
+    def load_tensor_host(self, tid: int, src: np.ndarray, stream=None) -> None:
+        """src: fp32 host array of the manifest shape [in, out] (staged through
+        the workspace; the call waits for the stream)."""
+        a = np.ascontiguousarray(src, dtype=np.float32)
+        check(lib().acid_model_load_tensor_host(self.h, tid, a.ctypes.data_as(C.c_void_p),
+                                                a.size, _stream(stream)))
 
     def load_weights(self, tensors: Iterable) -> None:
         """tensors: iterable of (id, name, fp32 numpy array) in any order."""

@@ -77,6 +77,8 @@ _SIGS = {
                                     C.POINTER(C.c_int64)]),
     "acid_model_create": (C.c_int, [C.POINTER(DitConfigC), _P, _P, C.c_int32, C.POINTER(_P)]),
     "acid_model_load_tensor": (C.c_int, [_P, C.c_int32, _P, C.c_int64, _P]),
+    "acid_model_load_tensor_host": (C.c_int, [_P, C.c_int32, _P, C.c_int64, _P]),
+    "acid_q_scale": (C.c_float, [C.c_int32]),
     "acid_model_destroy": (None, [_P]),
     "acid_model_set_timing": (C.c_int, [_P, C.c_int32]),
     "acid_model_reset_timing": (C.c_int, [_P]),

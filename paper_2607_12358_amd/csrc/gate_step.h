@@ -27,19 +27,19 @@ ACID_HD inline int32_t gate_step(acid_gate_state* st, const acid_gate_params* p,
   const int32_t step = st->step;
   st->step = step + 1;
   if (step < p->n_warmup) {
-    // Warmup: the base method runs the full model; the gate state is untouched.
+    // Leading steps of the base method: always run, state left as it was.
     *tau = __builtin_nan("");
     return 1;
   }
   st->sigma_sum = st->sigma_sum + s_t;
   const double adiff = __builtin_fabs(s_t - st->s_prev);
-  // Stable phase (small change of the signal): cache aggressively.
+  // A signal that moved by at most delta picks the larger threshold.
   const double t = (st->has_prev && adiff <= p->delta) ? p->tau_high : p->tau_low;
   int32_t compute;
   if (st->sigma_sum <= t) {
-    compute = 0;  // reuse the cached residual
+    compute = 0;
   } else {
-    compute = 1;  // run the model, reset the accumulator
+    compute = 1;  // a computed step restarts the accumulation
     st->sigma_sum = 0.0;
   }
   st->s_prev = s_t;

@@ -989,6 +989,48 @@ acid_status acid_model_load_tensor(acid_model* m, int32_t id, const float* src_d
   });
 }
 
+acid_status acid_model_load_tensor_host(acid_model* m, int32_t id, const float* src_host,
+                                        int64_t n, hipStream_t stream) {
+  if (!m || !src_host) return set_error(ACID_ERR_INVALID_ARG, "model and source must be non-NULL");
+  TensorInfo t;
+  ACID_TRY(tensor_info(m->cfg, id, &t));
+  const int64_t rows = t.d0, cols = t.rank == 2 ? t.d1 : 1;
+  if (n != rows * cols)
+    return set_error(ACID_ERR_SHAPE, "tensor %d has %lld elements, got %lld", id,
+                     (long long)(rows * cols), (long long)n);
+  char* dst = m->wb + t.off;
+  if (!t.gemm) {  // fp32 as given: one copy, host to arena
+    ACID_TRY(run(m, ACID_K_MISC, stream, "load tensor (host)", [&]() {
+      return hipMemcpyAsync(dst, src_host, (size_t)n * 4, hipMemcpyHostToDevice, stream);
+    }));
+    ACID_HIP(hipStreamSynchronize(stream));
+    return ACID_OK;
+  }
+  // GEMM weight: whole [in] rows of the [in][out] source are staged through
+  // the workspace's residual-stream buffer and transposed into columns
+  // i0 .. i0 + k of the [out][in] operand.
+  float* stage = m->kp(m->kl.h);
+  const int64_t stage_rows = (int64_t)(m->L() * m->H()) / cols;
+  if (stage_rows < 1) return set_error(ACID_ERR_SHAPE, "staging buffer smaller than one row");
+  const int64_t ldd = t.ldd ? t.ldd : rows;
+  const size_t es = esize(m->cfg.dtype);
+  for (int64_t i0 = 0; i0 < rows; i0 += stage_rows) {
+    const int64_t k = rows - i0 < stage_rows ? rows - i0 : stage_rows;
+    ACID_TRY(run(m, ACID_K_MISC, stream, "load tensor (host)", [&]() {
+      hipError_t e = hipMemcpyAsync(stage, src_host + i0 * cols, (size_t)(k * cols) * 4,
+                                    hipMemcpyHostToDevice, stream);
+      if (e != hipSuccess) return e;
+      return launch_transpose_convert(stage, k, cols, m->cfg.dtype, dst + (size_t)i0 * es, stream,
+                                      ldd);
+    }));
+    // the next chunk overwrites the staging buffer
+    ACID_HIP(hipStreamSynchronize(stream));
+  }
+  return ACID_OK;
+}
+
+float acid_q_scale(int32_t head_dim) { return head_dim > 0 ? attn_q_scale(head_dim) : 0.0f; }
+
 void acid_model_destroy(acid_model* m) {
   if (!m) return;
   // teardown: errors here have nowhere to go
@@ -1098,6 +1140,8 @@ acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K, const vo
           (int64_t)3 * epi->n_heads * epi->head_dim != N || epi->head_dim % 32)
         return set_error(ACID_ERR_SHAPE, "QKV: N must be 3 * n_heads * head_dim, head_dim % 32 == 0");
       if (epi->vt_ld < M) return set_error(ACID_ERR_SHAPE, "QKV: vt_ld < M");
+      if (epi->vt_ld % 8 || (uintptr_t)epi->vt % 16)
+        return set_error(ACID_ERR_INVALID_ARG, "QKV: vt must be 16-byte aligned, vt_ld % 8 == 0");
       break;
     case ACID_EPI_QKV_GELU: {
       if (!epi->q || !epi->k || !epi->vt || !epi->out)
@@ -1107,6 +1151,9 @@ acid_status acid_linear(int32_t dtype, int64_t M, int32_t N, int32_t K, const vo
         return set_error(ACID_ERR_SHAPE,
                          "QKV_GELU: 3 * n_heads * head_dim must be < N, head_dim % 32 == 0");
       if (epi->vt_ld < M) return set_error(ACID_ERR_SHAPE, "QKV_GELU: vt_ld < M");
+      if (epi->vt_ld % 8 || (uintptr_t)epi->vt % 16)
+        return set_error(ACID_ERR_INVALID_ARG,
+                         "QKV_GELU: vt must be 16-byte aligned, vt_ld % 8 == 0");
       if (epi->out_ld < N - nq) return set_error(ACID_ERR_SHAPE, "QKV_GELU: out_ld < N - 3 H");
       break;
     }

@@ -159,3 +159,18 @@ def test_c_gate_bit_exact_vs_oracle(lib):
         d2, t2, s2 = _c_gate_run(lib, list(s), p)
         assert d1 == d2, (k, list(s), p)
         assert _same(t1, t2) and _same(s1, s2), k
+
+
+def test_q_scale_is_the_documented_float(lib):
+    """acid_q_scale(d) is the fp32 value 1.4426950408889634f / sqrtf(d) the
+    header documents (log2(e)/sqrt(d) rounded to float)."""
+    import numpy as np
+    for d in (64, 128, 96, 1):
+        want = np.float32(np.float32(1.4426950408889634) / np.sqrt(np.float32(d)))
+        assert lib.acid_q_scale(d) == float(want)
+        assert abs(float(want) - math.log2(math.e) / math.sqrt(d)) <= 2 ** -23 * float(want)
+    assert lib.acid_q_scale(0) == 0.0
+
+
+def test_host_load_argument_errors(lib):
+    assert lib.acid_model_load_tensor_host(None, 0, None, 0, None) == L.ACID_ERR_INVALID_ARG

@@ -15,7 +15,8 @@ import torch
 
 import acid_inputs as ai
 import oracle as O
-from gpu_util import make_model, need_gpu, rel_err, to_dev, to_np
+from gpu_util import (BF16_U, assert_close_to_scale, assert_elementwise, attention_bound,
+                      make_model, need_gpu, rel_err, to_dev, to_np)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -62,6 +63,8 @@ def test_attention_fullsize_sampled(P, nh, L, d, prescaled):
         ref = O.attention(qj, kj, vj)
         got = to_np(o[rows, j * d:(j + 1) * d])
         assert rel_err(got, ref) < 1e-2, (j, rel_err(got, ref))
+        assert_elementwise(got, ref, attention_bound(qj, kj, vj), 1.05 * BF16_U,
+                           f"{nh}x{L}x{d} head {j}")
 
 
 GEMM_SHAPES = [  # (name, M, N, K, epilogue)
@@ -140,6 +143,7 @@ def test_block_fullsize_wan_sampled(P, wan_block):
     ref = om.block(h0, 0, mod6.astype(np.float64), rows=rows)
     got = to_np(h[rows])
     assert rel_err(got - h0[rows], ref - h0[rows]) < 2e-2
+    assert_close_to_scale(got - h0[rows], ref - h0[rows], True, "wan block")
     assert np.all(np.isfinite(to_np(h)))
 
 
@@ -164,6 +168,7 @@ def test_block_fullsize_cogvideox_sampled(P, block):
                                      [0, cfg.n_text - 1, cfg.n_text, cfg.n_tokens - 1]]))
     ref = om.block(h0, 0, mod6.astype(np.float64), rows=rows)
     assert rel_err(to_np(h[rows]) - h0[rows], ref - h0[rows]) < 2e-2
+    assert_close_to_scale(to_np(h[rows]) - h0[rows], ref - h0[rows], True, f"cogvideox {block} block")
     assert np.all(np.isfinite(to_np(h)))
 
 

@@ -13,7 +13,8 @@ import torch
 
 import acid_inputs as ai
 import oracle as O
-from gpu_util import bf16_values, make_model, need_gpu, rel_err, to_dev, to_np
+from gpu_util import (BF16_U, assert_elementwise, attention_bound, bf16_values, make_model,
+                      need_gpu, rel_err, to_dev, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -115,6 +116,11 @@ def test_attention_bf16(P, L, d, std, prescaled):
         e = rel_err(got, ref)
         assert e < 2e-2, (j, e)
         assert e < 1e-2  # typical bf16 P rounding error is ~3e-3
+        # and element by element, within the bound the bf16 rounding of the
+        # probabilities and of the output allows (a single wrong element,
+        # row or lane column fails here even when the head's norm hides it)
+        assert_elementwise(got, ref, attention_bound(q[j], k[j], v[j]), 1.05 * BF16_U,
+                           f"L={L} d={d} head {j}")
 
 
 @pytest.mark.parametrize("prescaled", [False, True], ids=["plain-q", "prescaled-q"])
@@ -124,7 +130,10 @@ def test_attention_f32(P, L, d, prescaled):
     nh = 3
     q, k, v, o = _attn_case(P, nh, L, d, torch.float32, 1.0, seed=L + d, prescaled=prescaled)
     for j in range(nh):
-        assert rel_err(o[:, j * d:(j + 1) * d], O.attention(q[j], k[j], v[j])) < 1e-5
+        ref = O.attention(q[j], k[j], v[j])
+        assert rel_err(o[:, j * d:(j + 1) * d], ref) < 1e-5
+        assert_elementwise(o[:, j * d:(j + 1) * d], ref, attention_bound(q[j], k[j], v[j], False),
+                           3e-5, f"fp32 L={L} d={d} head {j}")
 
 
 @pytest.mark.parametrize("prescaled", [False, True], ids=["plain-q", "prescaled-q"])
@@ -154,7 +163,10 @@ def test_attention_growing_and_spiking_scores(P, d, L, prescaled):
     got = to_np(o)
     assert np.all(np.isfinite(got))
     for j in range(nh):
-        assert rel_err(got[:, j * d:(j + 1) * d], O.attention(q[j], k[j], v[j])) < 1e-2
+        ref = O.attention(q[j], k[j], v[j])
+        assert rel_err(got[:, j * d:(j + 1) * d], ref) < 1e-2
+        assert_elementwise(got[:, j * d:(j + 1) * d], ref, attention_bound(q[j], k[j], v[j]),
+                           1.05 * BF16_U, f"growing scores L={L} d={d} head {j}")
 
 
 def test_attention_uniform_and_single_key(P):
@@ -186,27 +198,37 @@ def _linear_case(P, kind, M, N, K, dtype, seed):
     if dtype == torch.bfloat16:
         a, w = bf16_values(a), bf16_values(w)
     y = a.astype(np.float64) @ w.astype(np.float64) + b
+    # bound of the fp32 accumulation (exact products, K fp32 additions) per
+    # output, plus |b|: the element-wise check's absolute part
+    acc_err = K * 2.0 ** -24 * (np.abs(a).astype(np.float64) @ np.abs(w).astype(np.float64)
+                                + np.abs(b))
     ad, wtd, bd = to_dev(a, dtype), to_dev(w.T.copy(), dtype), to_dev(b)
     if kind == "bias":
         out = torch.empty((M, N), device="cuda")
         P.linear(ad, wtd, P.ACID_EPI_BIAS, bd, out=out)
-        return [(to_np(out), y, 1e-5)]
+        return [(to_np(out), y, 1e-5, acc_err)]
     if kind == "gelu":
         out = torch.empty((M, N), dtype=dtype, device="cuda")
         P.linear(ad, wtd, P.ACID_EPI_BIAS_GELU, bd, out=out)
-        return [(to_np(out), O.gelu_tanh(y), 1e-5 if dtype == torch.float32 else 4e-3)]
+        # GELU's slope is at most 1.13; its fp32 evaluation adds a few ulp
+        return [(to_np(out), O.gelu_tanh(y), 1e-5 if dtype == torch.float32 else 4e-3,
+                 1.13 * acc_err + 1e-6)]
     if kind == "gate_residual":
         h0 = rng.normal(size=(M, N)).astype(np.float32)
         g = rng.normal(size=N).astype(np.float32)
         h = to_dev(h0)
         P.linear(ad, wtd, P.ACID_EPI_GATE_RESIDUAL, bd, gate=to_dev(g), out=h)
-        return [(to_np(h) - h0, g * y, 1e-5)]
+        # plus the rounding of the fp32 update h + g y
+        return [(to_np(h) - h0, g * y, 1e-5,
+                 np.abs(g) * acc_err + 2.0 ** -23 * (np.abs(h0) + np.abs(g * y)))]
     if kind == "euler":
         x0 = rng.normal(size=(M, N)).astype(np.float32)
         x = to_dev(x0)
         v = torch.empty((M, N), device="cuda")
         P.linear(ad, wtd, P.ACID_EPI_EULER, bd, out=x, v_out=v, dsigma=-0.125)
-        return [(to_np(v), y, 1e-5), (to_np(x) - x0, -0.125 * y, 1e-5)]
+        return [(to_np(v), y, 1e-5, acc_err),
+                (to_np(x) - x0, -0.125 * y, 1e-5,
+                 0.125 * acc_err + 2.0 ** -23 * (np.abs(x0) + np.abs(0.125 * y)))]
     # qkv: N = 3 * heads * d; qkv_prescaled stores Q times log2(e)/sqrt(d)
     d = 64
     nh = N // (3 * d)
@@ -218,19 +240,32 @@ def _linear_case(P, kind, M, N, K, dtype, seed):
     pre = kind == "qkv_prescaled"
     P.linear(ad, wtd, P.ACID_EPI_QKV, bd, q=q, k=k, vt=vt, n_heads=nh, head_dim=d, q_prescale=pre)
     tol = 1e-5 if dtype == torch.float32 else 4e-3
-    yq = y[:, :H].reshape(M, nh, d).transpose(1, 0, 2) * (P.q_scale(d) if pre else 1.0)
+    c = P.q_scale(d) if pre else 1.0
+    yq = y[:, :H].reshape(M, nh, d).transpose(1, 0, 2) * c
     yk = y[:, H:2 * H].reshape(M, nh, d).transpose(1, 0, 2)
     yv = y[:, 2 * H:].reshape(M, nh, d).transpose(1, 2, 0)
-    return [(to_np(q), yq, tol), (to_np(k), yk, tol), (to_np(vt)[:, :, :M], yv, tol)]
+    eq = acc_err[:, :H].reshape(M, nh, d).transpose(1, 0, 2) * c + 2.0 ** -23 * np.abs(yq)
+    ek = acc_err[:, H:2 * H].reshape(M, nh, d).transpose(1, 0, 2)
+    ev = acc_err[:, 2 * H:].reshape(M, nh, d).transpose(1, 2, 0)
+    return [(to_np(q), yq, tol, eq), (to_np(k), yk, tol, ek), (to_np(vt)[:, :, :M], yv, tol, ev)]
+
+
+def _check_linear_elementwise(got, ref, atol, bf16_out, what):
+    """fp32 outputs: within the accumulation bound (and 2 ulp of the value);
+    bf16 outputs (GELU, Q, K, V): plus one bf16 rounding of the value."""
+    rtol = 1.01 * 2.0 ** -8 if bf16_out else 2.0 ** -22
+    assert_elementwise(got, ref, atol, rtol, what)
 
 
 @pytest.mark.parametrize("kind", KINDS)
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
 @pytest.mark.parametrize("M,N,K", [(1, 384, 128), (255, 384, 256), (300, 768, 384), (600, 384, 640), (513, 1152, 1536)])
 def test_linear(P, kind, dtype, M, N, K):
-    for got, ref, tol in _linear_case(P, kind, M, N, K, dtype, seed=M + N + K):
+    bf16_out = dtype == torch.bfloat16 and kind in ("gelu", "qkv", "qkv_prescaled")
+    for got, ref, tol, atol in _linear_case(P, kind, M, N, K, dtype, seed=M + N + K):
         e = rel_err(got, ref)
         assert e < tol, (kind, e)
+        _check_linear_elementwise(got, ref, atol, bf16_out, f"{kind} M={M} N={N} K={K}")
 
 
 @pytest.mark.parametrize("kind", KINDS)
@@ -240,8 +275,10 @@ def test_linear_large_tiles_ragged(P, kind):
     M, K = 8200, 256
     N = 2304 if kind.startswith("qkv") else 2176
     # the qkv case in _linear_case uses d = 64: 2304 = 3 x 12 x 64
-    for got, ref, tol in _linear_case(P, kind, M, N, K, torch.bfloat16, seed=17):
+    for got, ref, tol, atol in _linear_case(P, kind, M, N, K, torch.bfloat16, seed=17):
         assert rel_err(got, ref) < tol, kind
+        _check_linear_elementwise(got, ref, atol, kind in ("gelu", "qkv", "qkv_prescaled"),
+                                  f"{kind} M={M} N={N} K={K}")
 
 
 @pytest.mark.parametrize("d", [64, 128])

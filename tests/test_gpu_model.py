@@ -14,7 +14,7 @@ import torch
 
 import acid_inputs as ai
 import oracle as O
-from gpu_util import make_model, need_gpu, rel_err, to_dev, to_np
+from gpu_util import assert_close_to_scale, make_model, need_gpu, rel_err, to_dev, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +50,8 @@ def test_dit_step_f32(P, cfg, sigma):
     v, v_ref, r, r_ref = _step_case(P, cfg, sigma, std=0.1)
     assert rel_err(v, v_ref) < 1e-4
     assert rel_err(r, r_ref) < 1e-4
+    assert_close_to_scale(v, v_ref, False, f"{cfg.name} v")
+    assert_close_to_scale(r, r_ref, False, f"{cfg.name} residual")
 
 
 @pytest.mark.parametrize("cfg", [SMALL_BF16, SMALL_BF16_D64], ids=lambda c: c.name)
@@ -57,6 +59,8 @@ def test_dit_step_bf16(P, cfg):
     v, v_ref, r, r_ref = _step_case(P, cfg, 0.6, std=0.05)
     assert rel_err(v, v_ref) < 2e-2
     assert rel_err(r, r_ref) < 2e-2
+    assert_close_to_scale(v, v_ref, True, f"{cfg.name} v")
+    assert_close_to_scale(r, r_ref, True, f"{cfg.name} residual")
 
 
 def test_timestep_modulation(P):
@@ -215,3 +219,22 @@ def test_kernel_timer_counts_and_leaves_results_alone(P):
     assert tim["ln_mod"][1] == 2 * blocks + cfg.n_steps
     assert tim["gemm_head"][1] == cfg.n_steps
     assert tim["drift"][1] == cfg.n_steps
+
+
+@pytest.mark.parametrize("cfg", [ai.TINY, SMALL_BF16, SMALL_BF16.replace(name="small-par", block="parallel")],
+                         ids=lambda c: c.name)
+def test_host_pointer_load_matches_device_load(P, cfg):
+    """acid_model_load_tensor_host (fp32 [in][out] in host memory, staged
+    through the workspace in row chunks) fills the arena byte for byte as
+    acid_model_load_tensor does from a device copy."""
+    m1 = P.Model(cfg, max_steps=2)
+    m2 = P.Model(cfg, max_steps=2)
+    m1.arena.zero_()
+    m2.arena.zero_()
+    for tid, _name, w in ai.iter_weights(cfg):
+        m1.load_tensor(tid, torch.from_numpy(w).cuda())
+        m2.load_tensor_host(tid, w)
+    torch.cuda.synchronize()
+    assert torch.equal(m1.arena, m2.arena)
+    with pytest.raises(P.AcidError):
+        m2.load_tensor_host(0, np.zeros(3, np.float32))  # wrong element count

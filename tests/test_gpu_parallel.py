@@ -16,7 +16,8 @@ import torch
 
 import acid_inputs as ai
 import oracle as O
-from gpu_util import bf16_values, make_model, need_gpu, rel_err, to_dev, to_np
+from gpu_util import (assert_close_to_scale, bf16_values, make_model, need_gpu, rel_err,
+                      to_dev, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -128,6 +129,7 @@ def _block_case(P, cfg, seed=3):
 def test_block_parallel_vs_oracle(P, cfg, tol):
     got, ref = _block_case(P, cfg)
     assert rel_err(got, ref) < tol
+    assert_close_to_scale(got, ref, cfg.dtype == "bf16", f"{cfg.name} block")
 
 
 @pytest.mark.parametrize("cfg,tol", [(TINY_PAR, 1e-4), (SMALL_PAR, 2e-2)], ids=lambda c: getattr(c, "name", str(c)))
@@ -142,6 +144,8 @@ def test_dit_step_parallel_vs_oracle(P, cfg, tol):
     v_ref, h_ref = O.DiTModel(cfg, params).forward(x, 0.61, text)
     assert rel_err(to_np(v), v_ref) < tol
     assert rel_err(to_np(r), h_ref - x) < tol
+    assert_close_to_scale(to_np(v), v_ref, cfg.dtype == "bf16", f"{cfg.name} v")
+    assert_close_to_scale(to_np(r), h_ref - x, cfg.dtype == "bf16", f"{cfg.name} residual")
 
 
 def test_denoise_loop_parallel_vs_oracle(P):

@@ -89,3 +89,85 @@ def test_stack_without_text_equals_empty_text():
     cfg0 = CFG.replace(n_text=0)
     m0 = O.DiTModel(cfg0, m.p)
     np.testing.assert_array_equal(m0.stack(x, 0.2), m0.stack(x, 0.2, np.zeros((0, CFG.hidden))))
+
+
+# ------------------------------------------------ TEMNI (TeaCache's signal)
+#
+# Section 2, paragraph "TeaCache": the signal is formed from the noisy input
+# after LayerNorm and the timestep-embedding modulation of the first block,
+# i.e. block 0's first (shift, scale) pair.  With every adaLN weight at zero
+# the modulation vectors are the adaLN biases, known here independently of
+# the oracle's modulation code, and the LayerNorm is torch's.
+
+def _temni_pin_case():
+    H = CFG.hidden
+    p = ai.weights(CFG, std=0.2)
+    rng = np.random.default_rng(11)
+    for b in range(CFG.n_blocks):
+        p[f"blocks.{b}.ada.w"][:] = 0
+        p[f"blocks.{b}.ada.b"][:] = rng.normal(scale=0.5, size=6 * H).astype(np.float32)
+    x = rng.normal(size=(CFG.n_video, H)) * 3.0 + 1.5
+    return p, x
+
+
+def _temni_expected(p, x, block=0, shift_idx=0, scale_idx=1):
+    import torch
+    H = CFG.hidden
+    mod = p[f"blocks.{block}.ada.b"].astype(np.float64).reshape(6, H)
+    ln = torch.nn.functional.layer_norm(torch.from_numpy(x), (H,), eps=1e-6).numpy()
+    return ln * (1.0 + mod[scale_idx]) + mod[shift_idx]
+
+
+def _temni_pin_holds(model_cls) -> bool:
+    p, x = _temni_pin_case()
+    m = model_cls(CFG, p)
+    want = _temni_expected(p, x)
+    ok = True
+    for sigma in (1.0, 0.45, 0.0):
+        got = m.temni(x, sigma)
+        ok &= got.shape == want.shape and np.allclose(got, want, rtol=1e-12, atol=1e-12)
+    return bool(ok)
+
+
+def test_temni_is_block0_first_modulation_of_layer_norm():
+    assert _temni_pin_holds(O.DiTModel)
+    # the pin separates TEMNI from its near misses: the second triple, the
+    # pair swapped, another block's pair, the gate as shift, no LayerNorm
+    p, x = _temni_pin_case()
+    want = _temni_expected(p, x)
+    for other in (_temni_expected(p, x, 0, 3, 4), _temni_expected(p, x, 0, 1, 0),
+                  _temni_expected(p, x, 1), _temni_expected(p, x, 0, 2, 1)):
+        assert np.abs(other - want).max() > 0.1
+    mod = p["blocks.0.ada.b"].astype(np.float64).reshape(6, CFG.hidden)
+    assert np.abs(x * (1 + mod[1]) + mod[0] - want).max() > 0.1
+
+
+class _TemniSecondTriple(O.DiTModel):
+    def temni(self, x, sigma):
+        mod = self.modulation(sigma)["blocks"][0]
+        return O.modulate(O.layer_norm(x), mod[3], mod[4])
+
+
+class _TemniSwapped(O.DiTModel):
+    def temni(self, x, sigma):
+        mod = self.modulation(sigma)["blocks"][0]
+        return O.modulate(O.layer_norm(x), mod[1], mod[0])
+
+
+class _TemniBlock1(O.DiTModel):
+    def temni(self, x, sigma):
+        mod = self.modulation(sigma)["blocks"][1]
+        return O.modulate(O.layer_norm(x), mod[0], mod[1])
+
+
+class _TemniNoNorm(O.DiTModel):
+    def temni(self, x, sigma):
+        mod = self.modulation(sigma)["blocks"][0]
+        return O.modulate(np.asarray(x, np.float64), mod[0], mod[1])
+
+
+def test_temni_pin_rejects_planted_mistakes():
+    """Each plausible mistake in the oracle's TEMNI, planted in a subclass on
+    the CPU, fails the pin above."""
+    for bad in (_TemniSecondTriple, _TemniSwapped, _TemniBlock1, _TemniNoNorm):
+        assert not _temni_pin_holds(bad), bad.__name__
