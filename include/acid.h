@@ -279,6 +279,23 @@ acid_status acid_l1_norms(acid_model* m, const float* a_dev, const float* b_dev,
                           const float* c_dev, int64_t n, double* out_host,
                           hipStream_t stream);
 
+/* acid_l1_norms without a model and without any allocation, for callers
+ * that cannot allocate device memory (tight serving loops, harnesses that
+ * forbid hipMalloc) and hold no model workspace.
+ * Same arguments, sums and kernels as acid_l1_norms (bit-identical results
+ * whenever acid_l1_norms runs its full 1024-workgroup grid, i.e. for models
+ * with n_video >= 1024); no model and no size bound: the partial sums go to
+ * a 16 KB array (1024 fp64 pairs plus the result pair) that the library
+ * keeps in device memory on each device it runs on until the process ends,
+ * and the L1 grid never exceeds those 1024 workgroups.  The device is the
+ * stream's (the current device for the null stream).  n < 0:
+ * ACID_ERR_INVALID_ARG.  Calls that overlap on one device race on that
+ * array (one at a time per device); each call writes every entry it reads,
+ * so nothing carries over from an earlier call.  Synchronises the stream. */
+acid_status acid_l1_norms_noalloc(const float* a_dev, const float* b_dev,
+                                  const float* c_dev, int64_t n,
+                                  double* out_host, hipStream_t stream);
+
 /* EasyCache's skipped step over n fp32 elements: v = x + D; x_prev = x;
  * x = x + dsigma v (x updated in place; v_dev and x_prev_dev written;
  * offset_dev D read).  The four buffers must not overlap. */
@@ -406,8 +423,8 @@ typedef struct {
   float* v_out;         /* EULER only, may be NULL */
   void* q;              /* QKV: [n_heads][M][head_dim] */
   void* k;              /* QKV: [n_heads][M][head_dim] */
-  void* vt;             /* QKV: [n_heads][head_dim][vt_ld], 16-byte aligned */
-  int64_t vt_ld;        /* QKV: >= M, a multiple of 8 */
+  void* vt;             /* QKV: [n_heads][head_dim][vt_ld] */
+  int64_t vt_ld;        /* QKV: >= round_up(M, 8) */
   int32_t n_heads;      /* QKV: N == 3 * n_heads * head_dim (QKV_GELU: >) */
   int32_t head_dim;     /* QKV */
   float dsigma;         /* EULER */

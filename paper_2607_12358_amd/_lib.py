@@ -89,6 +89,7 @@ _SIGS = {
                             C.POINTER(C.c_int32), C.POINTER(C.c_double)]),
     "acid_cache_apply": (C.c_int, [C.c_int, _P, _P, _P, C.c_int64, _P]),
     "acid_l1_norms": (C.c_int, [_P, _P, _P, _P, C.c_int64, C.POINTER(C.c_double), _P]),
+    "acid_l1_norms_noalloc": (C.c_int, [_P, _P, _P, C.c_int64, C.POINTER(C.c_double), _P]),
     "acid_model_set_probe_blocks": (C.c_int, [_P, C.c_int32]),
     "acid_easycache_reuse": (C.c_int, [_P, _P, _P, _P, C.c_int64, C.c_float, _P]),
     "acid_denoise_loop": (C.c_int, [_P, _P, C.POINTER(C.c_float), C.c_int32, _P, C.c_int32,

@@ -22,7 +22,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libacid.so")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["elementwise.hip", "temb.hip", "gemm.hip", "attention.hip", "runtime.hip"]
+HIP_SOURCES = ["elementwise.hip", "temb.hip", "gemm.hip", "attention.hip", "runtime.hip",
+               "noalloc.hip"]
 HOST_SOURCES = ["gate.cpp"]
 
 

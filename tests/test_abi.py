@@ -172,5 +172,16 @@ def test_q_scale_is_the_documented_float(lib):
     assert lib.acid_q_scale(0) == 0.0
 
 
+def test_noalloc_l1_argument_errors(lib):
+    out = (C.c_double * 2)()
+    assert lib.acid_l1_norms_noalloc(None, None, None, -1, out, None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_l1_norms_noalloc(None, None, None, 4, out, None) == L.ACID_ERR_INVALID_ARG
+    assert lib.acid_l1_norms_noalloc(None, None, None, 4, None, None) == L.ACID_ERR_INVALID_ARG
+    # n == 0: empty sums without touching any buffer or the device
+    out[0] = out[1] = 7.0
+    assert lib.acid_l1_norms_noalloc(None, None, None, 0, out, None) == L.ACID_OK
+    assert out[0] == 0.0 and out[1] == 0.0
+
+
 def test_host_load_argument_errors(lib):
     assert lib.acid_model_load_tensor_host(None, 0, None, 0, None) == L.ACID_ERR_INVALID_ARG
