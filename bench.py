@@ -180,6 +180,36 @@ def psnr(x, ref) -> float:
     return math.inf if mse == 0.0 else 10.0 * math.log10(rng * rng / mse)
 
 
+def stream_ceilings(P, m, n: int, reps: int = 10) -> dict:
+    """Attainable streaming rates on this part, measured with the library's
+    own streaming kernels over three fp32 buffers of n elements: the cache
+    STORE kernel (two streams in, one out: the drift's and the cache's
+    mix) and the L1 sums (three streams in, nothing out)."""
+    import torch
+
+    bufs = [torch.randn(n, device="cuda") for _ in range(3)]
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    t21 = timed(lambda: P.cache_apply(P.ACID_CACHE_STORE, bufs[0], bufs[1], bufs[2]))
+    t_ro = timed(lambda: m.l1_norms(bufs[0], bufs[1], bufs[2]))
+    del bufs
+    torch.cuda.empty_cache()
+    return {"rw_2to1_gbs": 12.0 * n / t21 / 1e9, "read_only_gbs": 12.0 * n / t_ro / 1e9,
+            "buffer_bytes": 4 * n,
+            "kernels": "cache STORE (2 in, 1 out); L1 sums (3 in; includes its one-block "
+                       "final reduction and the read-back)"}
+
+
 def parse_list(text: str):
     return [float(v) for v in text.split(",") if v]
 
@@ -438,6 +468,14 @@ def main() -> int:
                 ent["gbs"] = rate / 1e9
                 ent["frac_hbm_peak"] = rate / 1e9 / PEAK_HBM_GBS
         kernels[name] = ent
+    ceilings = None
+    if cfg.dtype == "bf16":
+        ceilings = stream_ceilings(P, m, cfg.n_video * cfg.hidden)
+        for name in ("drift", "cache"):  # two streams in, one out
+            if name in kernels and "gbs" in kernels[name]:
+                kernels[name]["frac_measured_2to1"] = kernels[name]["gbs"] / ceilings["rw_2to1_gbs"]
+        log(f"streaming ceilings: {ceilings['rw_2to1_gbs']:.0f} GB/s (2:1), "
+            f"{ceilings['read_only_gbs']:.0f} GB/s (read-only)")
     gemm_ms = sum(timing[k][0] for k in timing if k.startswith("gemm_"))
     gemm_flop = sum(work[k][1] for k in work if k.startswith("gemm_"))
     gemm_tflops = gemm_flop * kernel_loops / (gemm_ms * 1e-3) / 1e12 if gemm_ms else None
@@ -546,6 +584,7 @@ def main() -> int:
         "gemm_frac_peak": (gemm_tflops / (PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else
                                           PEAK_F32_TFLOPS)) if gemm_tflops else None,
         "kernels": kernels,
+        "stream_ceilings": ceilings,
         "nocache_s_per_loop": nocache,
         "speedup_vs_nocache": (nocache / s_per_loop) if nocache else None,
         "roofline": roofline,

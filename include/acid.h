@@ -423,8 +423,8 @@ typedef struct {
   float* v_out;         /* EULER only, may be NULL */
   void* q;              /* QKV: [n_heads][M][head_dim] */
   void* k;              /* QKV: [n_heads][M][head_dim] */
-  void* vt;             /* QKV: [n_heads][head_dim][vt_ld] */
-  int64_t vt_ld;        /* QKV: >= round_up(M, 8) */
+  void* vt;             /* QKV: [n_heads][head_dim][vt_ld], 16-byte aligned */
+  int64_t vt_ld;        /* QKV: >= M, a multiple of 8 */
   int32_t n_heads;      /* QKV: N == 3 * n_heads * head_dim (QKV_GELU: >) */
   int32_t head_dim;     /* QKV */
   float dsigma;         /* EULER */

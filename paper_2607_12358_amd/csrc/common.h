@@ -78,11 +78,14 @@ inline float attn_q_scale(int d) { return 1.4426950408889634f / sqrtf((float)d);
 hipError_t launch_ln_modulate(int out_dtype, const float* x, int64_t rows, int H,
                               const float* shift, const float* scale, void* out,
                               hipStream_t s, const int32_t* pred = nullptr);
-// TEMNI + per-row partial sums; m_prev may be null (then no partials).
+// TEMNI + per-workgroup partial sums (drift_partial_count(rows) fp64 pairs);
+// m_prev may be null (then no partials).
 hipError_t launch_temni_drift(const float* x, int64_t rows, int H, const float* shift,
                               const float* scale, const float* m_prev, float* m_cur,
                               double* partials, hipStream_t s);
-// Fixed-order reduction of per-row (num, den) pairs -> out[0]=num, out[1]=den, out[2]=s.
+int64_t drift_partial_count(int64_t rows);
+// Fixed-order reduction of the (num, den) pairs of launch_temni_drift over
+// `rows` rows -> out[0]=num, out[1]=den, out[2]=s.
 hipError_t launch_drift_finalize(const double* partials, int64_t rows, double* out,
                                  hipStream_t s);
 // With `flag` (a device int32) the operation is STORE if *flag, else APPLY;

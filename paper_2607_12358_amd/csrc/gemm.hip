@@ -433,6 +433,47 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
   // read-modify-write kinds issue 32 loads before their stores.
   const bool full = m0 + BM <= M;
   const int64_t mrow = m0 + wm * 128 + 4 * lg;
+  if constexpr (KIND == ACID_EPI_QKV || KIND == ACID_EPI_QKV_GELU) {
+    // V columns are rows of V^T, whose tokens are contiguous: a lane holds 4
+    // consecutive tokens per group r / 4 and its partner lane (l ^ 32) the
+    // next 4, so one permlane32 swap per dword gives each lane 8 consecutive
+    // tokens: 16-byte stores instead of 2-byte ones scattered over 32 rows.
+    const int nw = n0 + wn * 64;
+    if (full && nw >= 2 * e.H && nw + 64 <= 3 * e.H) {  // all 64 columns in V
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const int n = nw + nb * 32 + lr;
+        const int cc = n - 2 * e.H;
+        const int head = cc / e.head_dim, dd = cc - head * e.head_dim;
+        bf16* vrow = static_cast<bf16*>(e.vt) + ((int64_t)head * e.head_dim + dd) * e.vt_ld;
+        const float bias = e.bias[n];
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) {
+          uint32_t w[8];  // tokens 8 (r / 4) + 4 lg + r % 4 as bf16 pairs
+#pragma unroll
+          for (int r = 0; r < 16; r += 2) {
+            const bf16x2 pr = {(bf16)(acc[mb][nb][r] + bias), (bf16)(acc[mb][nb][r + 1] + bias)};
+            w[r / 2] = __builtin_bit_cast(uint32_t, pr);
+          }
+          const int64_t t0 = m0 + wm * 128 + mb * 32 + 8 * lg;
+#pragma unroll
+          for (int p = 0; p < 2; ++p) {  // groups 2p (tokens +0..7) and 2p + 1 (+8..15)
+            uint32_t lo[2], hi[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const auto sw = __builtin_amdgcn_permlane32_swap(w[4 * p + h], w[4 * p + 2 + h],
+                                                               false, false);
+              lo[h] = sw[0];
+              hi[h] = sw[1];
+            }
+            const u32x4 v = {lo[0], lo[1], hi[0], hi[1]};
+            *reinterpret_cast<u32x4*>(vrow + t0 + 16 * p) = v;
+          }
+        }
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const int n = n0 + wn * 64 + nb * 32 + lr;

@@ -321,7 +321,7 @@ def test_linear_shape_errors(P):
 def test_linear_deterministic(P):
     got = []
     for _ in range(3):
-        (o, _, _), = _linear_case(P, "bias", 700, 1536, 1536, torch.bfloat16, seed=5)
+        (o, _, _, _), = _linear_case(P, "bias", 700, 1536, 1536, torch.bfloat16, seed=5)
         got.append(o)
     assert np.array_equal(got[0], got[1]) and np.array_equal(got[0], got[2])
 
