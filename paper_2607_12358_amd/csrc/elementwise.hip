@@ -123,11 +123,15 @@ __global__ __launch_bounds__(256) void temni_drift_kernel(
         y.z = (v[c].z - mean) * rstd * (1.f + sc.z) + sh.z;
         y.w = (v[c].w - mean) * rstd * (1.f + sc.w) + sh.w;
         if (m_prev) {
-          float4 p = *(mp4 + idx);
+          // m_prev and m_cur are read and written once per step, and the
+          // whole DiT step runs before they are touched again: both bypass
+          // the caches (non-temporal)
+          const f32x4 pv = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mp4) + idx);
+          const float4 p = make_float4(pv[0], pv[1], pv[2], pv[3]);
           num += (fabsf(y.x - p.x) + fabsf(y.y - p.y)) + (fabsf(y.z - p.z) + fabsf(y.w - p.w));
           den += (fabsf(p.x) + fabsf(p.y)) + (fabsf(p.z) + fabsf(p.w));
         }
-        *(mc4 + idx) = y;
+        __builtin_nontemporal_store(f32x4{y.x, y.y, y.z, y.w}, reinterpret_cast<f32x4*>(mc4) + idx);
       }
     }
     if (m_prev) {
