@@ -474,6 +474,23 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
       return;
     }
   }
+  if constexpr (!ColEpi<KIND, bf16>::kRmw) {
+    if (full) {
+      // The two 32-column blocks of a wave fill the two halves of the same
+      // 128-byte line of each output row (bf16): store them back to back so
+      // the line is complete in the L2 before it can be written back.
+      const ColEpi<KIND, bf16> c0(e, n0 + wn * 64 + lr, N), c1(e, n0 + wn * 64 + 32 + lr, N);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t m = mrow + mb * 32 + 8 * (r >> 2) + (r & 3);
+          c0.put(m, acc[mb][0][r]);
+          c1.put(m, acc[mb][1][r]);
+        }
+      return;
+    }
+  }
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const int n = n0 + wn * 64 + nb * 32 + lr;
