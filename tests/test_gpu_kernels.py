@@ -102,7 +102,7 @@ def _attn_case(P, n_heads, L, d, dtype, std, seed, prescaled=False):
 
 
 @pytest.mark.parametrize("prescaled", [False, True], ids=["plain-q", "prescaled-q"])
-@pytest.mark.parametrize("L", [1, 63, 64, 65, 130, 300, 1000])
+@pytest.mark.parametrize("L", [1, 63, 64, 65, 128, 130, 256, 300, 320, 1000])
 @pytest.mark.parametrize("d", [64, 128])
 @pytest.mark.parametrize("std", [1.0, 4.0])
 def test_attention_bf16(P, L, d, std, prescaled):
