@@ -54,9 +54,9 @@ __device__ __forceinline__ float gelu_tanh(float z) {
 // Same function for bf16 outputs: 0.5 z (1 + tanh(u)) == z / (1 + e^(-2u)),
 // one exp2 and one reciprocal (hardware approximations, ~1 ulp each).
 __device__ __forceinline__ float gelu_tanh_fast(float z) {
-  // -2 log2(e) sqrt(2/pi)
-  const float k = -2.302208198144325f;
-  const float t = k * z * __builtin_fmaf(0.044715f * z, z, 1.0f);
+  // -2 log2(e) sqrt(2/pi), and the same times 0.044715
+  const float k = -2.302208198144325f, kc = -0.10294324f;
+  const float t = z * __builtin_fmaf(kc * z, z, k);
   return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(t));
 }
 

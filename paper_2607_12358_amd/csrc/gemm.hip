@@ -490,6 +490,21 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
         }
       return;
     }
+    // The ragged last row tile: row offsets from mrow in 32 bits (a 64-bit
+    // row per element made the register allocator spill).
+    const int rows_left = (int)(M - mrow < 128 ? M - mrow : 128);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const ColEpi<KIND, bf16> ce(e, n0 + wn * 64 + nb * 32 + lr, N);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int dr = mb * 32 + 8 * (r >> 2) + (r & 3);
+          if (dr < rows_left) ce.put(mrow + dr, acc[mb][nb][r]);
+        }
+    }
+    return;
   }
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
