@@ -27,22 +27,31 @@ __device__ __forceinline__ void store4(bf16* out, int64_t idx4, float4 y) {
   reinterpret_cast<bf16x4*>(out)[idx4] = v;
 }
 
+// Chunk c of a row as this lane reads and writes it.  Indices past the
+// row's n4 chunks are clamped to its last chunk, so every load and store is
+// unconditional (a load under a branch that also uses it makes the wave
+// wait for each load in turn): such a lane holds a copy of the last chunk,
+// stores the same bytes as the lane that owns it, and is left out of the
+// row's sums.
+__device__ __forceinline__ int chunk_index(int lane, int c, int n4) {
+  const int idx = lane + 64 * c;
+  return idx < n4 ? idx : n4 - 1;
+}
+
 // Loads a row into registers and returns (mean, rstd) of LayerNorm
-// (biased variance, eps 1e-6).
+// (biased variance, eps 1e-6).  All of the row's loads are issued before
+// the first is used.
 template <int CPL>
 __device__ __forceinline__ void load_row_stats(const float4* __restrict__ xr, int n4, int lane,
                                                float4 (&v)[CPL], float& mean, float& rstd,
                                                int H) {
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) v[c] = xr[chunk_index(lane, c, n4)];
   float s = 0.f;
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
-    int idx = lane + 64 * c;
-    if (idx < n4) {
-      v[c] = *(xr + idx);
-      s += (v[c].x + v[c].y) + (v[c].z + v[c].w);
-    } else {
-      v[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+    const float t = (v[c].x + v[c].y) + (v[c].z + v[c].w);
+    s += lane + 64 * c < n4 ? t : 0.f;
   }
   s = wave_sum(s);
   mean = s / (float)H;
@@ -78,15 +87,14 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
   const float4* sc4 = reinterpret_cast<const float4*>(scale);
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
-    int idx = lane + 64 * c;
-    if (idx < n4) {
-      float4 sc = sc4[idx], sh = sh4[idx], y;
-      y.x = (v[c].x - mean) * rstd * (1.f + sc.x) + sh.x;
-      y.y = (v[c].y - mean) * rstd * (1.f + sc.y) + sh.y;
-      y.z = (v[c].z - mean) * rstd * (1.f + sc.z) + sh.z;
-      y.w = (v[c].w - mean) * rstd * (1.f + sc.w) + sh.w;
-      store4(out, row * n4 + idx, y);
-    }
+    const int j = chunk_index(lane, c, n4);
+    const float4 sc = sc4[j], sh = sh4[j];
+    float4 y;
+    y.x = (v[c].x - mean) * rstd * (1.f + sc.x) + sh.x;
+    y.y = (v[c].y - mean) * rstd * (1.f + sc.y) + sh.y;
+    y.z = (v[c].z - mean) * rstd * (1.f + sc.z) + sh.z;
+    y.w = (v[c].w - mean) * rstd * (1.f + sc.w) + sh.w;
+    store4(out, row * n4 + j, y);
   }
 }
 
@@ -113,27 +121,54 @@ __global__ __launch_bounds__(256) void temni_drift_kernel(
     const float4* sc4 = reinterpret_cast<const float4*>(scale);
     const float4* mp4 = reinterpret_cast<const float4*>(m_prev + row * H);
     float4* mc4 = reinterpret_cast<float4*>(m_cur + row * H);
+    // One straight-line body with the previous TEMNI, one without.  The
+    // m_cur stores may alias the loads as far as the compiler can tell, so
+    // each group of G chunks loads all it needs before its first store.
+    auto body = [&](auto with_prev) {
+      constexpr bool kPrev = decltype(with_prev)::value;
+      constexpr int G = CPL < 6 ? CPL : 6;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      int idx = lane + 64 * c;
-      if (idx < n4) {
-        float4 sc = sc4[idx], sh = sh4[idx], y;
-        y.x = (v[c].x - mean) * rstd * (1.f + sc.x) + sh.x;
-        y.y = (v[c].y - mean) * rstd * (1.f + sc.y) + sh.y;
-        y.z = (v[c].z - mean) * rstd * (1.f + sc.z) + sh.z;
-        y.w = (v[c].w - mean) * rstd * (1.f + sc.w) + sh.w;
-        if (m_prev) {
+      for (int c0 = 0; c0 < CPL; c0 += G) {
+        float4 sc[G], sh[G];
+        f32x4 pv[G];
+#pragma unroll
+        for (int i = 0; i < G && c0 + i < CPL; ++i) {
+          const int j = chunk_index(lane, c0 + i, n4);
+          sc[i] = sc4[j];
+          sh[i] = sh4[j];
           // m_prev and m_cur are read and written once per step, and the
           // whole DiT step runs before they are touched again: both bypass
           // the caches (non-temporal)
-          const f32x4 pv = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mp4) + idx);
-          const float4 p = make_float4(pv[0], pv[1], pv[2], pv[3]);
-          num += (fabsf(y.x - p.x) + fabsf(y.y - p.y)) + (fabsf(y.z - p.z) + fabsf(y.w - p.w));
-          den += (fabsf(p.x) + fabsf(p.y)) + (fabsf(p.z) + fabsf(p.w));
+          if constexpr (kPrev) pv[i] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mp4) + j);
         }
-        __builtin_nontemporal_store(f32x4{y.x, y.y, y.z, y.w}, reinterpret_cast<f32x4*>(mc4) + idx);
+        __builtin_amdgcn_sched_barrier(0);  // the group's loads stay ahead of its stores
+#pragma unroll
+        for (int i = 0; i < G && c0 + i < CPL; ++i) {
+          const int c = c0 + i;
+          const float4 v4 = v[c];
+          float4 y;
+          y.x = (v4.x - mean) * rstd * (1.f + sc[i].x) + sh[i].x;
+          y.y = (v4.y - mean) * rstd * (1.f + sc[i].y) + sh[i].y;
+          y.z = (v4.z - mean) * rstd * (1.f + sc[i].z) + sh[i].z;
+          y.w = (v4.w - mean) * rstd * (1.f + sc[i].w) + sh[i].w;
+          if constexpr (kPrev) {
+            const float4 p = make_float4(pv[i][0], pv[i][1], pv[i][2], pv[i][3]);
+            const float dn =
+                (fabsf(y.x - p.x) + fabsf(y.y - p.y)) + (fabsf(y.z - p.z) + fabsf(y.w - p.w));
+            const float dd = (fabsf(p.x) + fabsf(p.y)) + (fabsf(p.z) + fabsf(p.w));
+            const bool in = lane + 64 * c < n4;
+            num += in ? dn : 0.f;
+            den += in ? dd : 0.f;
+          }
+          __builtin_nontemporal_store(f32x4{y.x, y.y, y.z, y.w},
+                                      reinterpret_cast<f32x4*>(mc4) + chunk_index(lane, c, n4));
+        }
       }
-    }
+    };
+    if (m_prev)
+      body(std::true_type{});
+    else
+      body(std::false_type{});
     if (m_prev) {
       num = wave_sum(num);
       den = wave_sum(den);
