@@ -535,13 +535,32 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
             ce.put(mrow + mb * 32 + 8 * (r >> 2) + (r & 3), acc[mb][nb][r]);
       }
     } else {
+      // The ragged last row tile of a read-modify-write kind: loads from rows
+      // clamped to M - 1 (always valid) batched as above, stores guarded.  A
+      // load under the store's guard would wait for each element in turn.
+      const int rows_left = (int)(M - mrow < 128 ? M - mrow : 128);
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
+      for (int h = 0; h < 2; ++h) {
+        float prev[2][16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int64_t m = mrow + mb * 32 + 8 * (r >> 2) + (r & 3);
-          if (m < M) ce.put(m, acc[mb][nb][r]);
-        }
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int dr = (2 * h + mb) * 32 + 8 * (r >> 2) + (r & 3);
+            prev[mb][r] = ce.old(dr < rows_left ? mrow + dr : M - 1);
+          }
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) asm volatile("" ::"v"(prev[mb][r]));  // loads land here
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int dr = (2 * h + mb) * 32 + 8 * (r >> 2) + (r & 3);
+            if (dr < rows_left) ce.put_old(mrow + dr, acc[2 * h + mb][nb][r], prev[mb][r]);
+          }
+      }
     }
   }
 }
