@@ -496,6 +496,9 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
       const ColEpi<KIND, bf16> ce(e, n0 + wn * 64 + nb * 32 + lr, N);
+      // The column's bias has landed before the guarded stores: a load still
+      // in flight there makes every guarded block wait for all earlier stores.
+      asm volatile("" ::"v"(ce.bias));
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
