@@ -51,6 +51,23 @@ def _kernels_of(obj, tmp):
     return [k for k in kernels if "name" in k]
 
 
+def _waits_of(obj, tmp):
+    """Number of `s_waitcnt vmcnt(0)` per kernel in obj's gfx950 code (the
+    code object extracted by _kernels_of, disassembled)."""
+    co = os.path.join(tmp, os.path.basename(obj)) + ".co"
+    dis = subprocess.run([_tool("llvm-objdump"), "-d", "--no-show-raw-insn", co], check=True,
+                         capture_output=True, text=True).stdout
+    out, name = {}, None
+    for line in dis.splitlines():
+        m = re.match(r"^[0-9a-f]+ <(\S+)>:", line)
+        if m:
+            name = m.group(1)
+            out[name] = 0
+        elif name and "s_waitcnt vmcnt(0)" in line:
+            out[name] += 1
+    return out
+
+
 @pytest.fixture(scope="module")
 def kernels(tmp_path_factory):
     objs = sorted(glob.glob(os.path.join(BUILD, "*.o")))
@@ -63,6 +80,9 @@ def kernels(tmp_path_factory):
     for o in objs:
         ks = _kernels_of(o, tmp)
         if ks:
+            waits = _waits_of(o, tmp) if _tool("llvm-objdump") else {}
+            for k in ks:
+                k["vmcnt0"] = waits.get(k["name"])
             out[os.path.basename(o)] = ks
     return out
 
@@ -97,3 +117,24 @@ def test_matrix_kernels_fit_two_waves_per_simd(kernels):
                 if "gemm_bf16_kernel" in k["name"]:
                     assert int(k["group_segment_fixed_size"]) == 160 * 1024, k["name"]
     assert seen >= 10
+
+
+# Most full memory waits a hot kernel may contain.  A load under a bounds
+# guard together with its use (or a load still in flight where guarded
+# stores begin) turns into one wait per element, and such a kernel shows
+# tens to hundreds of them; batched kernels wait a handful of times.
+WAIT_BUDGET = {"gemm_bf16_kernel": 10, "attn_bf16_kernel": 8, "ln_modulate_kernel": 3,
+               "temni_drift_kernel": 4, "cache_kernel": 4, "l1_partials_kernel": 3}
+
+
+def test_hot_kernels_keep_memory_in_flight(kernels):
+    checked = 0
+    for ks in kernels.values():
+        for k in ks:
+            for key, budget in WAIT_BUDGET.items():
+                if key in k["name"] and k.get("vmcnt0") is not None:
+                    checked += 1
+                    assert k["vmcnt0"] <= budget, (k["name"], k["vmcnt0"], budget)
+    if checked == 0:
+        pytest.skip("llvm-objdump not found")
+    assert checked >= 30
