@@ -46,7 +46,8 @@ def test_cache_store_apply(P, n):
 # ------------------------------------------------------- LN + modulation
 
 
-@pytest.mark.parametrize("rows,H", [(1, 256), (37, 1024), (300, 1536), (5, 3072), (0, 256)])
+@pytest.mark.parametrize("rows,H", [(1, 256), (37, 1024), (300, 1536), (5, 3072), (0, 256),
+                                    (64, 100), (33, 1000), (7, 2052), (3, 4)])
 @pytest.mark.parametrize("out", ["f32", "bf16"])
 def test_ln_modulate(P, rows, H, out):
     rng = np.random.default_rng(rows * 7 + H)

@@ -75,7 +75,12 @@ def test_timestep_modulation(P):
         assert rel_err(tab[i], ref) < 1e-5
 
 
-@pytest.mark.parametrize("cfg", [ai.TINY, SMALL_BF16], ids=lambda c: c.name)
+# hidden 384: 96 float4 chunks per row, so 32 lanes of the second chunk
+# read a clamped copy of the row's last chunk
+TINY_384 = ai.TINY.replace(name="tiny-384", hidden=384, n_heads=6, ffn=768)
+
+
+@pytest.mark.parametrize("cfg", [ai.TINY, SMALL_BF16, TINY_384], ids=lambda c: c.name)
 def test_drift_signal(P, cfg):
     m, params = make_model(P, cfg, max_steps=4)
     om = O.DiTModel(cfg, params)
