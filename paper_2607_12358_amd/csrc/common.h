@@ -130,9 +130,13 @@ hipError_t launch_skinny_gemm(const float* X, int ldx, int S, int K, const float
                               int64_t y_stride, hipStream_t s);
 
 // GEMMs (gemm.hip)
+// split_ws: for bf16, a workspace of kGemmSplitWsBytes with which grids whose
+// last round would leave most CUs idle split those tiles along K (nullptr:
+// never split).
+constexpr size_t kGemmSplitWsBytes = (size_t)256 * 256 * 256 * 4;
 hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, const void* wt,
                          const acid_epilogue_args& epi, hipStream_t s,
-                         const int32_t* pred = nullptr);
+                         const int32_t* pred = nullptr, float* split_ws = nullptr);
 
 // Attention (attention.hip)
 // o_ld: row stride of O in elements (0: n_heads * d).

@@ -25,6 +25,8 @@
 //   of tiles that share activation rows.
 // fp32 path: a plain 64 x 64 register-blocked VALU kernel for the fp32
 //   configuration (small shapes, latency-bound).
+#include <atomic>
+
 #include "common.h"
 
 namespace acid {
@@ -48,6 +50,7 @@ struct Epi {
   int64_t out_ld;       // QKV_GELU: row stride of the GELU output
   int n_qkv;            // QKV_GELU: columns [0, n_qkv) are Q | K | V
   float q_mul;          // QKV kinds: factor on the Q columns (1: plain Q)
+  float* split_ws;      // bf16: fp32 partial tiles of a K split (nullptr: no split)
 };
 
 // Q | K | V head-major destination of column c < 3 H (which = c / H).
@@ -212,6 +215,8 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kWaves = 8;                // 2 (tokens) x 4 (features), two per SIMD
 constexpr int kTileElems = 256 * BK;     // one operand tile per stage (32 KB)
+constexpr int64_t kSplitItemFloats = 256 * 256;  // one K-split partial tile (256 KB)
+constexpr int64_t kSplitMaxItems = 256;           // work items the split workspace holds
 
 // One 16-byte-per-lane LDS-DMA: lane l reads 16 bytes at base + off(l) and
 // writes LDS bytes [lds + 16 l, +16).  base and lds are wave-uniform.
@@ -236,196 +241,13 @@ __device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
 }
 __device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
 
-// Operand tiles are 256 rows x 64 (K-contiguous 128-byte rows: every row
-// fetch is one whole line).  DMA instruction i (0..3) of wave w fills LDS
-// bytes [(4 w + i) KB, +1 KB) = rows 32 w + 8 i .. +7; lane l lands in row
-// 32 w + 8 i + l / 8, slot l % 8, which holds global chunk
-// (l % 8) ^ ((row / 2) % 8) (= (l % 8) ^ (l / 16) for even i, ^ 4 more for
-// odd i).  With 64 four-byte LDS banks a row spans half the banks, so 16
-// consecutive fragment rows read at one chunk cover all 64 banks once.
-//
-// Eight waves, two per SIMD: while one wave of a SIMD stalls issuing its
-// DMAs (a wave that issues global loads holds back its own MFMA issue), the
-// other keeps the MFMA unit busy.  Each wave owns 128 x 64 of the tile
-// (4 x 2 blocks of 32 x 32, 128 accumulator registers).
+// Epilogue of one 256 x 256 tile: wave (wm, wn) stores its 128 x 64 block
+// from the MFMA accumulators.
 template <int KIND>
-__global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A, const bf16* Wt,
-                                                                   int64_t M, int N, int K,
-                                                                   Epi e) {
-  if (e.pred && *e.pred == 0) return;
-  // Three A tiles and two B tiles, one LDS object per tile so the compiler
-  // can tell the tile being read from the tile being filled.
-  __shared__ __attribute__((aligned(1024))) bf16 As0[kTileElems], Bs0[kTileElems];
-  __shared__ __attribute__((aligned(1024))) bf16 As1[kTileElems], Bs1[kTileElems];
-  __shared__ __attribute__((aligned(1024))) bf16 As2[kTileElems];
-
-  const int tiles_n = (N + BN - 1) / BN;
-  const int64_t tiles_m = (M + BM - 1) / BM;
-  int64_t tm;
-  int tn;
-  tile_coords(xcd_remap(blockIdx.x, tiles_m * tiles_n), tiles_m, tiles_n, tm, tn);
-  const int64_t m0 = tm * BM;
-  const int n0 = tn * BN;
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 2, wn = wave & 3;
+__device__ __forceinline__ void tile_epilogue(const Epi& e, f32x16 (&acc)[4][2], int64_t M,
+                                              int N, int64_t m0, int n0, int wm, int wn,
+                                              int lane) {
   const int lr = lane & 31, lg = lane >> 5;
-  // A tile of width 128 at the right edge (N % 256 == 128): waves with
-  // wn >= 2 compute on clamped rows and store nothing.
-  const bool active = n0 + wn * 64 < N;
-
-  // Load-side addressing: byte offsets from the tile's first row (rows past
-  // the edge are clamped; they only feed outputs that are never stored).
-  // The K offset of a stage is added to the scalar base, so the per-lane
-  // offsets stay fixed and a DMA needs no vector arithmetic.
-  const int chunk_even = (lane & 7) ^ (lane >> 4);
-  const int chunk_odd = (lane & 7) ^ ((lane >> 4) ^ 4);
-  const uint64_t a_base = uniform_ptr(A + m0 * K);
-  const uint64_t b_base = uniform_ptr(Wt + (int64_t)n0 * K);
-  uint32_t a_off[4], b_off[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = wave * 32 + i * 8 + (lane >> 3);
-    const int ra = m0 + r < M ? r : (int)(M - 1 - m0);
-    const int rb = n0 + r < N ? r : N - 1 - n0;
-    const int ch = (i & 1) ? chunk_odd : chunk_even;
-    a_off[i] = (uint32_t)(ra * K + ch * 8) * 2u;
-    b_off[i] = (uint32_t)(rb * K + ch * 8) * 2u;
-  }
-  const uint32_t lds_wave = (uint32_t)(wave * 4 * 1024);
-  auto lds_addr = [&](const bf16* tile) {
-    return (uint32_t)(uintptr_t)(lds_void_t*)tile + lds_wave;
-  };
-
-  // Read-side addressing: fragment row rr at K-step kk (16 wide) reads chunk
-  // 2 kk + lg, stored at slot (2 kk + lg) ^ ((rr / 2) % 8), and
-  // (rr / 2) % 8 == (lr / 2) % 8 for every fragment row of this lane.
-  const int a_rbase = (wm * 128 + lr) * BK;
-  const int b_rbase = (wn * 64 + lr) * BK;
-  int sl[4];
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) sl[kk] = 8 * ((2 * kk + lg) ^ ((lr >> 1) & 7));
-
-  f32x16 acc[4][2];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
-  auto read_frags = [&](const bf16* As, const bf16* Bs, int slot, bf16x8(&fa)[4],
-                        bf16x8(&fb)[2]) {
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-      fa[mb] = *reinterpret_cast<const bf16x8*>(As + a_rbase + mb * 32 * BK + slot);
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-      fb[nb] = *reinterpret_cast<const bf16x8*>(Bs + b_rbase + nb * 32 * BK + slot);
-  };
-  auto mma = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2]) {
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
-  };
-  auto load_stage = [&](const bf16* As, const bf16* Bs, int k0) {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
-    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(b_base + (uint32_t)(k0 * 2), b_off[i], lb + i * 1024);
-  };
-  // The last K-step of a stage with the refill of its tiles interleaved: one
-  // DMA after each of the 8 MFMAs (order pinned by scheduling barriers), the
-  // weight tile (K offset kb) first, the activation tile (ka) last.
-  auto mma_refill = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2], const bf16* As,
-                        const bf16* Bs, int ka, int kb) {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
-    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
-    const uint64_t ak = a_base + (uint32_t)(ka * 2), bk = b_base + (uint32_t)(kb * 2);
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
-        const int j = mb * 2 + nb, i = j & 3;
-        if (j < 4)
-          dma16(bk, b_off[i], lb + i * 1024);
-        else
-          dma16(ak, a_off[i], la + i * 1024);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-  };
-  auto load_a = [&](const bf16* As, int k0) {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
-#pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
-  };
-
-  const int KT = K / BK;  // even: K % 128 == 0
-  auto kc = [&](int k) { return (k < KT ? k : KT - 1) * BK; };
-  // Three A stages and two B stages (160 KB): the activations, streamed from
-  // HBM, are fetched two stages ahead, the weights one.  Prologue: A 0, B 0,
-  // A 1, B 1, A 2 in flight; stage 0 landed (vmcnt 12).
-  load_stage(As0, Bs0, 0);
-  load_stage(As1, Bs1, kc(1));
-  load_a(As2, kc(2));
-  __builtin_amdgcn_s_waitcnt((12 & 15) | (7 << 4) | (15 << 8));
-  __builtin_amdgcn_s_barrier();
-  read_frags(As0, Bs0, sl[0], fa0, fb0);
-
-  // Stage kt reads A[kt % 3], B[kt % 2]; in its last K-step it refills
-  // B[kt % 2] with stage kt + 2 and then A[kt % 3] with stage kt + 3.  At
-  // its barrier the group issued last (A of stage kt + 2) may still be in
-  // flight: vmcnt(4).
-  int kt = 0;
-#define GEMM_STAGE(AS, BS, AN, BN_)                                              \
-  {                                                                            \
-    read_frags(AS, BS, sl[1], fa1, fb1);                                       \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    mma(fa0, fb0);                                                             \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    read_frags(AS, BS, sl[2], fa0, fb0);                                       \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    mma(fa1, fb1);                                                             \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    read_frags(AS, BS, sl[3], fa1, fb1);                                       \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    mma(fa0, fb0);                                                             \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    __builtin_amdgcn_s_waitcnt(4 | (7 << 4) | (0 << 8));                       \
-    __builtin_amdgcn_s_barrier();                                              \
-    read_frags(AN, BN_, sl[0], fa0, fb0);                                      \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    mma_refill(fa1, fb1, AS, BS, kc(kt + 3), kc(kt + 2));                      \
-    __builtin_amdgcn_sched_barrier(0);                                         \
-    ++kt;                                                                      \
-  }
-  while (kt + 6 <= KT) {
-    GEMM_STAGE(As0, Bs0, As1, Bs1)
-    GEMM_STAGE(As1, Bs1, As2, Bs0)
-    GEMM_STAGE(As2, Bs0, As0, Bs1)
-    GEMM_STAGE(As0, Bs1, As1, Bs0)
-    GEMM_STAGE(As1, Bs0, As2, Bs1)
-    GEMM_STAGE(As2, Bs1, As0, Bs0)
-  }
-  if (kt + 2 <= KT) {
-    GEMM_STAGE(As0, Bs0, As1, Bs1)
-    GEMM_STAGE(As1, Bs1, As2, Bs0)
-  }
-  if (kt + 2 <= KT) {
-    GEMM_STAGE(As2, Bs0, As0, Bs1)
-    GEMM_STAGE(As0, Bs1, As1, Bs0)
-  }
-#undef GEMM_STAGE
-  wait_all();  // the last refill lands before the workgroup's LDS is released
-  if (!active) return;
-
   // D[i][j] of a 32x32 block: j = lane % 32, i = 8 (r / 4) + 4 (lane / 32) + r % 4.
   // A lane owns one feature column per 32-wide block: set up its epilogue
   // once, then handle its 64 rows of that column.  Full tiles skip the row
@@ -568,6 +390,267 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
   }
 }
 
+// Operand tiles are 256 rows x 64 (K-contiguous 128-byte rows: every row
+// fetch is one whole line).  DMA instruction i (0..3) of wave w fills LDS
+// bytes [(4 w + i) KB, +1 KB) = rows 32 w + 8 i .. +7; lane l lands in row
+// 32 w + 8 i + l / 8, slot l % 8, which holds global chunk
+// (l % 8) ^ ((row / 2) % 8) (= (l % 8) ^ (l / 16) for even i, ^ 4 more for
+// odd i).  With 64 four-byte LDS banks a row spans half the banks, so 16
+// consecutive fragment rows read at one chunk cover all 64 banks once.
+//
+// Eight waves, two per SIMD: while one wave of a SIMD stalls issuing its
+// DMAs (a wave that issues global loads holds back its own MFMA issue), the
+// other keeps the MFMA unit busy.  Each wave owns 128 x 64 of the tile
+// (4 x 2 blocks of 32 x 32, 128 accumulator registers).
+//
+// K split (grids whose last round of tiles would leave most CUs idle): the
+// first tiles_main work items are whole tiles in the XCD-aware order; each of
+// the remaining tiles is split into `split` equal K ranges, one work item
+// each, which store their raw fp32 partial sums to e.split_ws for
+// gemm_split_reduce_kernel.
+template <int KIND>
+__global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A, const bf16* Wt,
+                                                                   int64_t M, int N, int K,
+                                                                   Epi e, int64_t tiles_main,
+                                                                   int split) {
+  if (e.pred && *e.pred == 0) return;
+  // Three A tiles and two B tiles, one LDS object per tile so the compiler
+  // can tell the tile being read from the tile being filled.
+  __shared__ __attribute__((aligned(1024))) bf16 As0[kTileElems], Bs0[kTileElems];
+  __shared__ __attribute__((aligned(1024))) bf16 As1[kTileElems], Bs1[kTileElems];
+  __shared__ __attribute__((aligned(1024))) bf16 As2[kTileElems];
+
+  const int tiles_n = (N + BN - 1) / BN;
+  const int64_t tiles_m = (M + BM - 1) / BM;
+  int64_t tm;
+  int tn;
+  int64_t item = -1;  // K-split work item, or -1 for a whole tile
+  int kbeg = 0, klen = K;
+  if ((int64_t)blockIdx.x < tiles_main) {
+    tile_coords(xcd_remap(blockIdx.x, tiles_main), tiles_m, tiles_n, tm, tn);
+  } else {
+    item = (int64_t)blockIdx.x - tiles_main;
+    klen = K / split;
+    kbeg = (int)(item % split) * klen;
+    tile_coords(tiles_main + item / split, tiles_m, tiles_n, tm, tn);
+  }
+  const int64_t m0 = tm * BM;
+  const int n0 = tn * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  const int lr = lane & 31, lg = lane >> 5;
+  // A tile of width 128 at the right edge (N % 256 == 128): waves with
+  // wn >= 2 compute on clamped rows and store nothing.
+  const bool active = n0 + wn * 64 < N;
+
+  // Load-side addressing: byte offsets from the tile's first row (rows past
+  // the edge are clamped; they only feed outputs that are never stored).
+  // The K offset of a stage is added to the scalar base, so the per-lane
+  // offsets stay fixed and a DMA needs no vector arithmetic.
+  const int chunk_even = (lane & 7) ^ (lane >> 4);
+  const int chunk_odd = (lane & 7) ^ ((lane >> 4) ^ 4);
+  const uint64_t a_base = uniform_ptr(A + m0 * K + kbeg);
+  const uint64_t b_base = uniform_ptr(Wt + (int64_t)n0 * K + kbeg);
+  uint32_t a_off[4], b_off[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = wave * 32 + i * 8 + (lane >> 3);
+    const int ra = m0 + r < M ? r : (int)(M - 1 - m0);
+    const int rb = n0 + r < N ? r : N - 1 - n0;
+    const int ch = (i & 1) ? chunk_odd : chunk_even;
+    a_off[i] = (uint32_t)(ra * K + ch * 8) * 2u;
+    b_off[i] = (uint32_t)(rb * K + ch * 8) * 2u;
+  }
+  const uint32_t lds_wave = (uint32_t)(wave * 4 * 1024);
+  auto lds_addr = [&](const bf16* tile) {
+    return (uint32_t)(uintptr_t)(lds_void_t*)tile + lds_wave;
+  };
+
+  // Read-side addressing: fragment row rr at K-step kk (16 wide) reads chunk
+  // 2 kk + lg, stored at slot (2 kk + lg) ^ ((rr / 2) % 8), and
+  // (rr / 2) % 8 == (lr / 2) % 8 for every fragment row of this lane.
+  const int a_rbase = (wm * 128 + lr) * BK;
+  const int b_rbase = (wn * 64 + lr) * BK;
+  int sl[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) sl[kk] = 8 * ((2 * kk + lg) ^ ((lr >> 1) & 7));
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
+  auto read_frags = [&](const bf16* As, const bf16* Bs, int slot, bf16x8(&fa)[4],
+                        bf16x8(&fb)[2]) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+      fa[mb] = *reinterpret_cast<const bf16x8*>(As + a_rbase + mb * 32 * BK + slot);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+      fb[nb] = *reinterpret_cast<const bf16x8*>(Bs + b_rbase + nb * 32 * BK + slot);
+  };
+  auto mma = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2]) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+  };
+  auto load_stage = [&](const bf16* As, const bf16* Bs, int k0) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(b_base + (uint32_t)(k0 * 2), b_off[i], lb + i * 1024);
+  };
+  // The last K-step of a stage with the refill of its tiles interleaved: one
+  // DMA after each of the 8 MFMAs (order pinned by scheduling barriers), the
+  // weight tile (K offset kb) first, the activation tile (ka) last.
+  auto mma_refill = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2], const bf16* As,
+                        const bf16* Bs, int ka, int kb) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
+    const uint64_t ak = a_base + (uint32_t)(ka * 2), bk = b_base + (uint32_t)(kb * 2);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
+        const int j = mb * 2 + nb, i = j & 3;
+        if (j < 4)
+          dma16(bk, b_off[i], lb + i * 1024);
+        else
+          dma16(ak, a_off[i], la + i * 1024);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  };
+  auto load_a = [&](const bf16* As, int k0) {
+    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
+  };
+
+  const int KT = klen / BK;  // even: K and each split's K range are multiples of 128
+  auto kc = [&](int k) { return (k < KT ? k : KT - 1) * BK; };
+  // Three A stages and two B stages (160 KB): the activations, streamed from
+  // HBM, are fetched two stages ahead, the weights one.  Prologue: A 0, B 0,
+  // A 1, B 1, A 2 in flight; stage 0 landed (vmcnt 12).
+  load_stage(As0, Bs0, 0);
+  load_stage(As1, Bs1, kc(1));
+  load_a(As2, kc(2));
+  __builtin_amdgcn_s_waitcnt((12 & 15) | (7 << 4) | (15 << 8));
+  __builtin_amdgcn_s_barrier();
+  read_frags(As0, Bs0, sl[0], fa0, fb0);
+
+  // Stage kt reads A[kt % 3], B[kt % 2]; in its last K-step it refills
+  // B[kt % 2] with stage kt + 2 and then A[kt % 3] with stage kt + 3.  At
+  // its barrier the group issued last (A of stage kt + 2) may still be in
+  // flight: vmcnt(4).
+  int kt = 0;
+#define GEMM_STAGE(AS, BS, AN, BN_)                                              \
+  {                                                                            \
+    read_frags(AS, BS, sl[1], fa1, fb1);                                       \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma(fa0, fb0);                                                             \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    read_frags(AS, BS, sl[2], fa0, fb0);                                       \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma(fa1, fb1);                                                             \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    read_frags(AS, BS, sl[3], fa1, fb1);                                       \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma(fa0, fb0);                                                             \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    __builtin_amdgcn_s_waitcnt(4 | (7 << 4) | (0 << 8));                       \
+    __builtin_amdgcn_s_barrier();                                              \
+    read_frags(AN, BN_, sl[0], fa0, fb0);                                      \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    mma_refill(fa1, fb1, AS, BS, kc(kt + 3), kc(kt + 2));                      \
+    __builtin_amdgcn_sched_barrier(0);                                         \
+    ++kt;                                                                      \
+  }
+  while (kt + 6 <= KT) {
+    GEMM_STAGE(As0, Bs0, As1, Bs1)
+    GEMM_STAGE(As1, Bs1, As2, Bs0)
+    GEMM_STAGE(As2, Bs0, As0, Bs1)
+    GEMM_STAGE(As0, Bs1, As1, Bs0)
+    GEMM_STAGE(As1, Bs0, As2, Bs1)
+    GEMM_STAGE(As2, Bs1, As0, Bs0)
+  }
+  if (kt + 2 <= KT) {
+    GEMM_STAGE(As0, Bs0, As1, Bs1)
+    GEMM_STAGE(As1, Bs1, As2, Bs0)
+  }
+  if (kt + 2 <= KT) {
+    GEMM_STAGE(As2, Bs0, As0, Bs1)
+    GEMM_STAGE(As0, Bs1, As1, Bs0)
+  }
+#undef GEMM_STAGE
+  wait_all();  // the last refill lands before the workgroup's LDS is released
+  if (!active) return;
+  if (item >= 0) {
+    // Partial sums of this K range: value q of thread tid at (q * 512 + tid)
+    // float4s into the item's 256 KB (consecutive threads, consecutive 16 B).
+    f32x4* dst = reinterpret_cast<f32x4*>(e.split_ws) + item * (kSplitItemFloats / 4);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int q = (mb * 2 + nb) * 4 + r4;
+          dst[q * 64 * kWaves + tid] = f32x4{acc[mb][nb][4 * r4], acc[mb][nb][4 * r4 + 1],
+                                             acc[mb][nb][4 * r4 + 2], acc[mb][nb][4 * r4 + 3]};
+        }
+    return;
+  }
+  tile_epilogue<KIND>(e, acc, M, N, m0, n0, wm, wn, lane);
+}
+
+// The split tiles: partial sums added in split order (deterministic), then
+// the tile's epilogue.  Work item b reduces tile tiles_main + b.
+template <int KIND>
+__global__ __launch_bounds__(64 * kWaves, 1) void gemm_split_reduce_kernel(int64_t M, int N, Epi e,
+                                                                           int64_t tiles_main,
+                                                                           int split) {
+  if (e.pred && *e.pred == 0) return;
+  const int tiles_n = (N + BN - 1) / BN;
+  const int64_t tiles_m = (M + BM - 1) / BM;
+  int64_t tm;
+  int tn;
+  tile_coords(tiles_main + blockIdx.x, tiles_m, tiles_n, tm, tn);
+  const int64_t m0 = tm * BM;
+  const int n0 = tn * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+  if (!(n0 + wn * 64 < N)) return;
+  const f32x4* src = reinterpret_cast<const f32x4*>(e.split_ws) +
+                     (int64_t)blockIdx.x * split * (kSplitItemFloats / 4);
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int q = (mb * 2 + nb) * 4 + r4;
+        f32x4 v = src[q * 64 * kWaves + tid];
+        for (int sp = 1; sp < split; ++sp)
+          v += src[sp * (kSplitItemFloats / 4) + q * 64 * kWaves + tid];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[mb][nb][4 * r4 + i] = v[i];
+      }
+  tile_epilogue<KIND>(e, acc, M, N, m0, n0, wm, wn, lane);
+}
+
 // ------------------------------------------------------------ fp32 VALU
 
 template <int KIND>
@@ -618,13 +701,54 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
   }
 }
 
+// K split of the last round's tiles: when the tiles beyond whole rounds of
+// the device's CUs would leave at least half of them idle, those `rem` tiles
+// are split into S K ranges (S <= 8, S * rem within the CUs and the 256 work
+// items the workspace holds, each range a multiple of 128).  Each range is at
+// least 2048 long: a work item also fills the staging ring and writes its
+// 256 KB of partial sums, which the reduction reads back, and with shorter
+// ranges that costs more than the fuller round saves (measured: split into
+// K ranges of 256-1024, the small configuration's GEMMs ran twice as long).
+int cu_count() {
+  static std::atomic<int> cus{0};
+  int c = cus.load(std::memory_order_relaxed);
+  if (c == 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        c < 1)
+      c = 256;
+    cus.store(c, std::memory_order_relaxed);
+  }
+  return c;
+}
+int choose_split(int64_t tiles, int K, int64_t& rem) {
+  const int cus = cu_count();
+  rem = tiles % cus;
+  if (rem == 0 || 2 * rem > cus) return 1;
+  int S = (int)(cus / rem);
+  if (S > 8) S = 8;
+  while (S > 1 && (rem * S > kSplitMaxItems || K % (S * 128) != 0 || K / S < 2048)) --S;
+  return S;
+}
+
 template <int KIND>
 hipError_t launch_kind(int dtype, int64_t M, int N, int K, const void* a, const void* wt,
                        const Epi& e, hipStream_t s) {
   if (dtype == ACID_BF16) {
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    hipLaunchKernelGGL(gemm_bf16_kernel<KIND>, dim3((unsigned)tiles), dim3(64 * kWaves), 0, s,
-                       (const bf16*)a, (const bf16*)wt, M, N, K, e);
+    int64_t rem = 0;
+    const int split = e.split_ws ? choose_split(tiles, K, rem) : 1;
+    const int64_t tiles_main = tiles - (split > 1 ? rem : 0);
+    const int64_t grid = tiles_main + (split > 1 ? rem * split : 0);
+    hipLaunchKernelGGL(gemm_bf16_kernel<KIND>, dim3((unsigned)grid), dim3(64 * kWaves), 0, s,
+                       (const bf16*)a, (const bf16*)wt, M, N, K, e, tiles_main, split);
+    if (split > 1) {
+      const hipError_t err = hipGetLastError();
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL(gemm_split_reduce_kernel<KIND>, dim3((unsigned)rem), dim3(64 * kWaves),
+                         0, s, M, N, e, tiles_main, split);
+    }
   } else {
     dim3 grid((unsigned)((M + 63) / 64), (unsigned)(N / 64));
     hipLaunchKernelGGL(gemm_f32_kernel<KIND>, grid, dim3(256), 0, s, (const float*)a,
@@ -636,9 +760,11 @@ hipError_t launch_kind(int dtype, int64_t M, int N, int K, const void* a, const 
 }  // namespace
 
 hipError_t launch_linear(int dtype, int64_t M, int N, int K, const void* a, const void* wt,
-                         const acid_epilogue_args& ea, hipStream_t s, const int32_t* pred) {
+                         const acid_epilogue_args& ea, hipStream_t s, const int32_t* pred,
+                         float* split_ws) {
   if (M == 0) return hipSuccess;
   Epi e;
+  e.split_ws = dtype == ACID_BF16 ? split_ws : nullptr;
   e.bias = ea.bias;
   e.gate = ea.gate;
   e.out = ea.out;

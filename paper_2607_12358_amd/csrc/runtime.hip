@@ -147,6 +147,7 @@ struct WorkLayout {
   size_t h, act, q, k, vt, o, g, modtab, temb_e, temb_hid, temb_u, partials, dres, m0, m1, r, v;
   size_t dtrace, gstate;  // device-resident gate: per-step trace, state
   size_t dskip, ecst;     // per-step skip words; EasyCache (k, have k, |dx|)
+  size_t splitk;          // bf16: the GEMMs' K-split partial tiles
   size_t total;
   int64_t vt_ld;
 };
@@ -185,6 +186,7 @@ WorkLayout work_layout(const acid_dit_config& c, int max_steps) {
   W.gstate = put(sizeof(acid_gate_state));
   W.dskip = put(S * sizeof(int32_t));
   W.ecst = put(4 * sizeof(double));
+  W.splitk = put(c.dtype == ACID_BF16 ? kGemmSplitWsBytes : 0);
   W.total = off;
   return W;
 }
@@ -243,6 +245,8 @@ struct acid_model {
   T* bp(int b, size_t off) const { return reinterpret_cast<T*>(wb + wl.blk0 + (size_t)b * wl.blk_stride + off); }
   template <class T = float>
   T* kp(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+  // The GEMMs' K-split workspace (bf16 models; fp32 GEMMs never split).
+  float* split_ws() const { return cfg.dtype == ACID_BF16 ? kp<float>(kl.splitk) : nullptr; }
 };
 
 namespace {
@@ -358,7 +362,7 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   e.head_dim = c.head_dim;
   e.q_prescale = 1;  // Q leaves the GEMM in the softmax's exp2 units
   ACID_TRY(run(m, ACID_K_GEMM_QKV, s, "qkv gemm", [&]() {
-    return launch_linear(dt, L, 3 * H, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred);
+    return launch_linear(dt, L, 3 * H, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred, m->split_ws());
   }));
   ACID_TRY(run(m, ACID_K_ATTENTION, s, "attention", [&]() {
     return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, o, s, pred, 0,
@@ -370,7 +374,7 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   p.gate = mod6 + 2 * H;
   p.out = h;
   ACID_TRY(run(m, ACID_K_GEMM_PROJ, s, "proj gemm", [&]() {
-    return launch_linear(dt, L, H, H, o, m->bp<void>(b, m->wl.o_w), p, s, pred);
+    return launch_linear(dt, L, H, H, o, m->bp<void>(b, m->wl.o_w), p, s, pred, m->split_ws());
   }));
   ACID_TRY(ln_mod(m, h, L, mod6 + 3 * H, mod6 + 4 * H, act, s, pred));
   acid_epilogue_args f1 = {};
@@ -378,7 +382,7 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   f1.bias = m->bp(b, m->wl.f1_b);
   f1.out = g;
   ACID_TRY(run(m, ACID_K_GEMM_FFN1, s, "ffn1 gemm", [&]() {
-    return launch_linear(dt, L, F, H, act, m->bp<void>(b, m->wl.f1_w), f1, s, pred);
+    return launch_linear(dt, L, F, H, act, m->bp<void>(b, m->wl.f1_w), f1, s, pred, m->split_ws());
   }));
   acid_epilogue_args f2 = {};
   f2.kind = ACID_EPI_GATE_RESIDUAL;
@@ -386,7 +390,7 @@ acid_status block_forward(acid_model* m, int b, const float* mod6, float* h, hip
   f2.gate = mod6 + 5 * H;
   f2.out = h;
   ACID_TRY(run(m, ACID_K_GEMM_FFN2, s, "ffn2 gemm", [&]() {
-    return launch_linear(dt, L, H, F, g, m->bp<void>(b, m->wl.f2_w), f2, s, pred);
+    return launch_linear(dt, L, H, F, g, m->bp<void>(b, m->wl.f2_w), f2, s, pred, m->split_ws());
   }));
   return ACID_OK;
 }
@@ -417,7 +421,7 @@ acid_status block_forward_parallel(acid_model* m, int b, const float* mod6, floa
   e.out_ld = H + F;
   e.q_prescale = 1;
   ACID_TRY(run(m, ACID_K_GEMM_QKV, s, "qkv+mlp gemm", [&]() {
-    return launch_linear(dt, L, 3 * H + F, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred);
+    return launch_linear(dt, L, 3 * H + F, H, act, m->bp<void>(b, m->wl.qkv_w), e, s, pred, m->split_ws());
   }));
   ACID_TRY(run(m, ACID_K_ATTENTION, s, "attention", [&]() {
     return launch_attention(dt, c.n_heads, L, c.head_dim, e.q, e.k, e.vt, e.vt_ld, g, s, pred,
@@ -430,7 +434,7 @@ acid_status block_forward_parallel(acid_model* m, int b, const float* mod6, floa
   p.gate = mod6 + 2 * H;
   p.out = h;
   return run(m, ACID_K_GEMM_PROJ, s, "attn+mlp projection gemm", [&]() {
-    return launch_linear(dt, L, H, H + F, g, m->bp<void>(b, m->wl.o_w), p, s, pred);
+    return launch_linear(dt, L, H, H + F, g, m->bp<void>(b, m->wl.o_w), p, s, pred, m->split_ws());
   });
 }
 
@@ -500,7 +504,7 @@ acid_status head_forward(acid_model* m, const float* row, const float* hv, float
     e.out = v_out;
   }
   return run(m, ACID_K_GEMM_HEAD, s, "head gemm", [&]() {
-    return launch_linear(c.dtype, m->Lv(), H, H, act, m->wp<void>(m->wl.head_w), e, s, pred);
+    return launch_linear(c.dtype, m->Lv(), H, H, act, m->wp<void>(m->wl.head_w), e, s, pred, m->split_ws());
   });
 }
 
