@@ -23,6 +23,9 @@ SMALL_BF16 = ai.DiTConfig("small-bf16-ragged", n_blocks=2, hidden=256, n_heads=2
                           ffn=640, n_video=300, n_text=7, dtype="bf16", n_steps=8)
 SMALL_BF16_D64 = SMALL_BF16.replace(name="small-bf16-d64", n_heads=4, head_dim=64, n_text=0,
                                     n_video=257)
+# FFN 4096 over 2 row tiles: the second FFN GEMM (K = 4096) splits its tiles
+# into two K ranges with a fixed-order reduction of the partial sums
+SMALL_BF16_SPLIT = SMALL_BF16.replace(name="small-bf16-ksplit", ffn=4096)
 
 
 @pytest.fixture(scope="module")
@@ -54,13 +57,31 @@ def test_dit_step_f32(P, cfg, sigma):
     assert_close_to_scale(r, r_ref, False, f"{cfg.name} residual")
 
 
-@pytest.mark.parametrize("cfg", [SMALL_BF16, SMALL_BF16_D64], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [SMALL_BF16, SMALL_BF16_D64, SMALL_BF16_SPLIT],
+                         ids=lambda c: c.name)
 def test_dit_step_bf16(P, cfg):
     v, v_ref, r, r_ref = _step_case(P, cfg, 0.6, std=0.05)
     assert rel_err(v, v_ref) < 2e-2
     assert rel_err(r, r_ref) < 2e-2
     assert_close_to_scale(v, v_ref, True, f"{cfg.name} v")
     assert_close_to_scale(r, r_ref, True, f"{cfg.name} residual")
+
+
+def test_dit_step_bf16_k_split_is_deterministic(P):
+    """The K-split GEMM's reduction adds the partial sums in a fixed order:
+    repeated steps are bit-identical."""
+    cfg = SMALL_BF16_SPLIT
+    m, _ = make_model(P, cfg, max_steps=4, std=0.05)
+    xd = to_dev(ai.latents(cfg))
+    td = to_dev(ai.text_tokens(cfg))
+    outs = []
+    for _ in range(3):
+        r = torch.empty_like(xd)
+        v = m.dit_step(xd, 0.6, td, resid=r)
+        torch.cuda.synchronize()
+        outs.append((to_np(v), to_np(r)))
+    for v, r in outs[1:]:
+        assert np.array_equal(v, outs[0][0]) and np.array_equal(r, outs[0][1])
 
 
 def test_timestep_modulation(P):
