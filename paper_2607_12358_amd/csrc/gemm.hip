@@ -14,8 +14,8 @@
 //   refill DMA and the next stage's first fragment reads hide behind its
 //   MFMAs; all other fragment reads are software-pipelined one sub-step
 //   ahead.  A wave that issues global loads holds back its own MFMA issue,
-//   so two waves share each SIMD: one keeps the MFMA unit busy while the
-//   other issues its DMAs.  A 256 x 256 tile halves the operand bytes per
+//   so two waves share each SIMD and one of them issues the DMAs of both:
+//   the other only reads fragments and issues MFMAs.  A 256 x 256 tile halves the operand bytes per
 //   flop of a 256 x 128 tile (operand traffic also costs clock under the
 //   power cap).  The activation tile feeds MFMA operand A and the weight
 //   tile operand B, so the accumulator holds C with lanes along features:
@@ -26,6 +26,7 @@
 // fp32 path: a plain 64 x 64 register-blocked VALU kernel for the fp32
 //   configuration (small shapes, latency-bound).
 #include <atomic>
+#include <type_traits>
 
 #include "common.h"
 
@@ -398,10 +399,10 @@ __device__ __forceinline__ void tile_epilogue(const Epi& e, f32x16 (&acc)[4][2],
 // odd i).  With 64 four-byte LDS banks a row spans half the banks, so 16
 // consecutive fragment rows read at one chunk cover all 64 banks once.
 //
-// Eight waves, two per SIMD: while one wave of a SIMD stalls issuing its
-// DMAs (a wave that issues global loads holds back its own MFMA issue), the
-// other keeps the MFMA unit busy.  Each wave owns 128 x 64 of the tile
-// (4 x 2 blocks of 32 x 32, 128 accumulator registers).
+// Eight waves, two per SIMD (waves w and w + 4): wave w issues the DMAs of
+// both (a wave that issues global loads holds back its own MFMA issue), so
+// wave w + 4 keeps the MFMA unit busy while wave w stalls.  Each wave owns
+// 128 x 64 of the tile (4 x 2 blocks of 32 x 32, 128 accumulator registers).
 //
 // K split (grids whose last round of tiles would leave most CUs idle): the
 // first tiles_main work items are whole tiles in the XCD-aware order; each of
@@ -448,24 +449,30 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
   // Load-side addressing: byte offsets from the tile's first row (rows past
   // the edge are clamped; they only feed outputs that are never stored).
   // The K offset of a stage is added to the scalar base, so the per-lane
-  // offsets stay fixed and a DMA needs no vector arithmetic.
+  // offsets stay fixed and a DMA needs no vector arithmetic.  Waves w and
+  // w + 4 share a SIMD: wave w (< 4) issues the DMAs of both (DMA i < 4 its
+  // own rows, i >= 4 those of wave w + 4), so wave w + 4 issues MFMAs only.
+  const bool dma_wave = wave < 4;
   const int chunk_even = (lane & 7) ^ (lane >> 4);
   const int chunk_odd = (lane & 7) ^ ((lane >> 4) ^ 4);
   const uint64_t a_base = uniform_ptr(A + m0 * K + kbeg);
   const uint64_t b_base = uniform_ptr(Wt + (int64_t)n0 * K + kbeg);
-  uint32_t a_off[4], b_off[4];
+  uint32_t a_off[8], b_off[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = wave * 32 + i * 8 + (lane >> 3);
+  for (int i = 0; i < 8; ++i) {
+    const int ww = (wave & 3) + (i >> 2) * 4;
+    const int r = ww * 32 + (i & 3) * 8 + (lane >> 3);
     const int ra = m0 + r < M ? r : (int)(M - 1 - m0);
     const int rb = n0 + r < N ? r : N - 1 - n0;
     const int ch = (i & 1) ? chunk_odd : chunk_even;
     a_off[i] = (uint32_t)(ra * K + ch * 8) * 2u;
     b_off[i] = (uint32_t)(rb * K + ch * 8) * 2u;
   }
-  const uint32_t lds_wave = (uint32_t)(wave * 4 * 1024);
-  auto lds_addr = [&](const bf16* tile) {
-    return (uint32_t)(uintptr_t)(lds_void_t*)tile + lds_wave;
+  auto tile_lds = [&](const bf16* tile) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)tile);
+  };
+  auto lds_slot = [&](int i) {
+    return (uint32_t)((((wave & 3) + (i >> 2) * 4) * 4 + (i & 3)) * 1024);
   };
 
   // Read-side addressing: fragment row rr at K-step kk (16 wide) reads chunk
@@ -503,57 +510,64 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
   };
   auto load_stage = [&](const bf16* As, const bf16* Bs, int k0) {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
-    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
+    const uint32_t la = tile_lds(As), lb = tile_lds(Bs);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
+    for (int i = 0; i < 8; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + lds_slot(i));
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(b_base + (uint32_t)(k0 * 2), b_off[i], lb + i * 1024);
+    for (int i = 0; i < 8; ++i) dma16(b_base + (uint32_t)(k0 * 2), b_off[i], lb + lds_slot(i));
   };
-  // The last K-step of a stage with the refill of its tiles interleaved: one
-  // DMA after each of the 8 MFMAs (order pinned by scheduling barriers), the
+  // The last K-step of a stage with the refill of its tiles interleaved: two
+  // DMAs after each of the 8 MFMAs (order pinned by scheduling barriers), the
   // weight tile (K offset kb) first, the activation tile (ka) last.
   auto mma_refill = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2], const bf16* As,
                         const bf16* Bs, int ka, int kb) {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
-    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(Bs));
+    const uint32_t la = tile_lds(As), lb = tile_lds(Bs);
     const uint64_t ak = a_base + (uint32_t)(ka * 2), bk = b_base + (uint32_t)(kb * 2);
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) {
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
-        const int j = mb * 2 + nb, i = j & 3;
-        if (j < 4)
-          dma16(bk, b_off[i], lb + i * 1024);
-        else
-          dma16(ak, a_off[i], la + i * 1024);
+        const int j = mb * 2 + nb;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int i = (2 * j + h) & 7;
+          if (j < 4)
+            dma16(bk, b_off[i], lb + lds_slot(i));
+          else
+            dma16(ak, a_off[i], la + lds_slot(i));
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
   };
   auto load_a = [&](const bf16* As, int k0) {
-    const uint32_t la = __builtin_amdgcn_readfirstlane(lds_addr(As));
+    const uint32_t la = tile_lds(As);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + i * 1024);
+    for (int i = 0; i < 8; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + lds_slot(i));
   };
 
   const int KT = klen / BK;  // even: K and each split's K range are multiples of 128
   auto kc = [&](int k) { return (k < KT ? k : KT - 1) * BK; };
   // Three A stages and two B stages (160 KB): the activations, streamed from
   // HBM, are fetched two stages ahead, the weights one.  Prologue: A 0, B 0,
-  // A 1, B 1, A 2 in flight; stage 0 landed (vmcnt 12).
-  load_stage(As0, Bs0, 0);
-  load_stage(As1, Bs1, kc(1));
-  load_a(As2, kc(2));
-  __builtin_amdgcn_s_waitcnt((12 & 15) | (7 << 4) | (15 << 8));
-  __builtin_amdgcn_s_barrier();
-  read_frags(As0, Bs0, sl[0], fa0, fb0);
+  // A 1, B 1, A 2 in flight (16 + 16 + 8 DMAs in a DMA wave); stage 0 landed
+  // (vmcnt 24; a wave without DMAs has nothing outstanding).
+  auto main_loop = [&](auto dma_flag) {
+    constexpr bool kDma = decltype(dma_flag)::value;
+    if constexpr (kDma) {
+      load_stage(As0, Bs0, 0);
+      load_stage(As1, Bs1, kc(1));
+      load_a(As2, kc(2));
+    }
+    __builtin_amdgcn_s_waitcnt((24 & 15) | (7 << 4) | (15 << 8) | ((24 >> 4) << 14));
+    __builtin_amdgcn_s_barrier();
+    read_frags(As0, Bs0, sl[0], fa0, fb0);
 
-  // Stage kt reads A[kt % 3], B[kt % 2]; in its last K-step it refills
-  // B[kt % 2] with stage kt + 2 and then A[kt % 3] with stage kt + 3.  At
-  // its barrier the group issued last (A of stage kt + 2) may still be in
-  // flight: vmcnt(4).
-  int kt = 0;
+    // Stage kt reads A[kt % 3], B[kt % 2]; in its last K-step it refills
+    // B[kt % 2] with stage kt + 2 and then A[kt % 3] with stage kt + 3.  At
+    // its barrier the group issued last (A of stage kt + 2, 8 DMAs) may still
+    // be in flight: vmcnt(8).
+    int kt = 0;
 #define GEMM_STAGE(AS, BS, AN, BN_)                                              \
   {                                                                            \
     read_frags(AS, BS, sl[1], fa1, fb1);                                       \
@@ -568,31 +582,39 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
     __builtin_amdgcn_sched_barrier(0);                                         \
     mma(fa0, fb0);                                                             \
     __builtin_amdgcn_sched_barrier(0);                                         \
-    __builtin_amdgcn_s_waitcnt(4 | (7 << 4) | (0 << 8));                       \
+    __builtin_amdgcn_s_waitcnt(8 | (7 << 4) | (0 << 8));                       \
     __builtin_amdgcn_s_barrier();                                              \
     read_frags(AN, BN_, sl[0], fa0, fb0);                                      \
     __builtin_amdgcn_sched_barrier(0);                                         \
-    mma_refill(fa1, fb1, AS, BS, kc(kt + 3), kc(kt + 2));                      \
+    if constexpr (kDma)                                                        \
+      mma_refill(fa1, fb1, AS, BS, kc(kt + 3), kc(kt + 2));                    \
+    else                                                                       \
+      mma(fa1, fb1);                                                           \
     __builtin_amdgcn_sched_barrier(0);                                         \
     ++kt;                                                                      \
   }
-  while (kt + 6 <= KT) {
-    GEMM_STAGE(As0, Bs0, As1, Bs1)
-    GEMM_STAGE(As1, Bs1, As2, Bs0)
-    GEMM_STAGE(As2, Bs0, As0, Bs1)
-    GEMM_STAGE(As0, Bs1, As1, Bs0)
-    GEMM_STAGE(As1, Bs0, As2, Bs1)
-    GEMM_STAGE(As2, Bs1, As0, Bs0)
-  }
-  if (kt + 2 <= KT) {
-    GEMM_STAGE(As0, Bs0, As1, Bs1)
-    GEMM_STAGE(As1, Bs1, As2, Bs0)
-  }
-  if (kt + 2 <= KT) {
-    GEMM_STAGE(As2, Bs0, As0, Bs1)
-    GEMM_STAGE(As0, Bs1, As1, Bs0)
-  }
+    while (kt + 6 <= KT) {
+      GEMM_STAGE(As0, Bs0, As1, Bs1)
+      GEMM_STAGE(As1, Bs1, As2, Bs0)
+      GEMM_STAGE(As2, Bs0, As0, Bs1)
+      GEMM_STAGE(As0, Bs1, As1, Bs0)
+      GEMM_STAGE(As1, Bs0, As2, Bs1)
+      GEMM_STAGE(As2, Bs1, As0, Bs0)
+    }
+    if (kt + 2 <= KT) {
+      GEMM_STAGE(As0, Bs0, As1, Bs1)
+      GEMM_STAGE(As1, Bs1, As2, Bs0)
+    }
+    if (kt + 2 <= KT) {
+      GEMM_STAGE(As2, Bs0, As0, Bs1)
+      GEMM_STAGE(As0, Bs1, As1, Bs0)
+    }
 #undef GEMM_STAGE
+  };
+  if (dma_wave)
+    main_loop(std::true_type{});
+  else
+    main_loop(std::false_type{});
   wait_all();  // the last refill lands before the workgroup's LDS is released
   if (!active) return;
   if (item >= 0) {
