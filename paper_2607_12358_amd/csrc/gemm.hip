@@ -516,63 +516,55 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
 #pragma unroll
     for (int i = 0; i < 8; ++i) dma16(b_base + (uint32_t)(k0 * 2), b_off[i], lb + lds_slot(i));
   };
-  // The last K-step of a stage with the refill of its tiles interleaved: two
-  // DMAs after each of the 8 MFMAs (order pinned by scheduling barriers), the
-  // weight tile (K offset kb) first, the activation tile (ka) last.
-  auto mma_refill = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2], const bf16* As,
-                        const bf16* Bs, int ka, int kb) {
-    const uint32_t la = tile_lds(As), lb = tile_lds(Bs);
-    const uint64_t ak = a_base + (uint32_t)(ka * 2), bk = b_base + (uint32_t)(kb * 2);
+  // One DMA after each of the 8 MFMAs of a K-step (order pinned by
+  // scheduling barriers): the 8 DMAs that fill tile T at K offset k0.
+  auto mma_dma = [&](const bf16x8(&fa)[4], const bf16x8(&fb)[2], const bf16* T,
+                     uint64_t base, const uint32_t(&off)[8], int k0) {
+    const uint32_t lt = tile_lds(T);
+    const uint64_t bk = base + (uint32_t)(k0 * 2);
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb) {
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mb], fb[nb], acc[mb][nb], 0, 0, 0);
-        const int j = mb * 2 + nb;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int i = (2 * j + h) & 7;
-          if (j < 4)
-            dma16(bk, b_off[i], lb + lds_slot(i));
-          else
-            dma16(ak, a_off[i], la + lds_slot(i));
-        }
+        const int i = mb * 2 + nb;
+        dma16(bk, off[i], lt + lds_slot(i));
         __builtin_amdgcn_sched_barrier(0);
       }
-  };
-  auto load_a = [&](const bf16* As, int k0) {
-    const uint32_t la = tile_lds(As);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) dma16(a_base + (uint32_t)(k0 * 2), a_off[i], la + lds_slot(i));
   };
 
   const int KT = klen / BK;  // even: K and each split's K range are multiples of 128
   auto kc = [&](int k) { return (k < KT ? k : KT - 1) * BK; };
-  // Three A stages and two B stages (160 KB): the activations, streamed from
-  // HBM, are fetched two stages ahead, the weights one.  Prologue: A 0, B 0,
-  // A 1, B 1, A 2 in flight (16 + 16 + 8 DMAs in a DMA wave); stage 0 landed
-  // (vmcnt 24; a wave without DMAs has nothing outstanding).
+  // Three A stages and two B stages (160 KB).  Stage kt refills A with
+  // stage kt + 2 during its first K-step (the buffer stage kt - 1 read) and
+  // B with stage kt + 2 during its last (the buffer it has just read), one
+  // DMA per MFMA, so the activations, streamed from HBM, are requested about
+  // 1.75 stages ahead of use and the weights 1.25.  Prologue: A 0, B 0, A 1,
+  // B 1 (32 DMAs in a DMA wave); stage 0 landed (vmcnt 16; a wave without
+  // DMAs has nothing outstanding).
   auto main_loop = [&](auto dma_flag) {
     constexpr bool kDma = decltype(dma_flag)::value;
     if constexpr (kDma) {
       load_stage(As0, Bs0, 0);
       load_stage(As1, Bs1, kc(1));
-      load_a(As2, kc(2));
     }
-    __builtin_amdgcn_s_waitcnt((24 & 15) | (7 << 4) | (15 << 8) | ((24 >> 4) << 14));
+    __builtin_amdgcn_s_waitcnt((16 & 15) | (7 << 4) | (15 << 8) | ((16 >> 4) << 14));
     __builtin_amdgcn_s_barrier();
     read_frags(As0, Bs0, sl[0], fa0, fb0);
 
-    // Stage kt reads A[kt % 3], B[kt % 2]; in its last K-step it refills
-    // B[kt % 2] with stage kt + 2 and then A[kt % 3] with stage kt + 3.  At
-    // its barrier the group issued last (A of stage kt + 2, 8 DMAs) may still
-    // be in flight: vmcnt(8).
+    // Stage kt reads A[kt % 3], B[kt % 2].  At its barrier the DMAs of this
+    // stage's first K-step (A of stage kt + 2) may still be in flight, those
+    // of stage kt + 1 (A in stage kt - 1, B in stage kt - 1's last K-step)
+    // have landed: vmcnt(8).
     int kt = 0;
-#define GEMM_STAGE(AS, BS, AN, BN_)                                              \
+#define GEMM_STAGE(AS, BS, AN, BN_, AP)                                          \
   {                                                                            \
     read_frags(AS, BS, sl[1], fa1, fb1);                                       \
     __builtin_amdgcn_sched_barrier(0);                                         \
-    mma(fa0, fb0);                                                             \
+    if constexpr (kDma)                                                        \
+      mma_dma(fa0, fb0, AP, a_base, a_off, kc(kt + 2));                        \
+    else                                                                       \
+      mma(fa0, fb0);                                                           \
     __builtin_amdgcn_sched_barrier(0);                                         \
     read_frags(AS, BS, sl[2], fa0, fb0);                                       \
     __builtin_amdgcn_sched_barrier(0);                                         \
@@ -587,27 +579,27 @@ __global__ __launch_bounds__(64 * kWaves, 1) void gemm_bf16_kernel(const bf16* A
     read_frags(AN, BN_, sl[0], fa0, fb0);                                      \
     __builtin_amdgcn_sched_barrier(0);                                         \
     if constexpr (kDma)                                                        \
-      mma_refill(fa1, fb1, AS, BS, kc(kt + 3), kc(kt + 2));                    \
+      mma_dma(fa1, fb1, BS, b_base, b_off, kc(kt + 2));                        \
     else                                                                       \
       mma(fa1, fb1);                                                           \
     __builtin_amdgcn_sched_barrier(0);                                         \
     ++kt;                                                                      \
   }
     while (kt + 6 <= KT) {
-      GEMM_STAGE(As0, Bs0, As1, Bs1)
-      GEMM_STAGE(As1, Bs1, As2, Bs0)
-      GEMM_STAGE(As2, Bs0, As0, Bs1)
-      GEMM_STAGE(As0, Bs1, As1, Bs0)
-      GEMM_STAGE(As1, Bs0, As2, Bs1)
-      GEMM_STAGE(As2, Bs1, As0, Bs0)
+      GEMM_STAGE(As0, Bs0, As1, Bs1, As2)
+      GEMM_STAGE(As1, Bs1, As2, Bs0, As0)
+      GEMM_STAGE(As2, Bs0, As0, Bs1, As1)
+      GEMM_STAGE(As0, Bs1, As1, Bs0, As2)
+      GEMM_STAGE(As1, Bs0, As2, Bs1, As0)
+      GEMM_STAGE(As2, Bs1, As0, Bs0, As1)
     }
     if (kt + 2 <= KT) {
-      GEMM_STAGE(As0, Bs0, As1, Bs1)
-      GEMM_STAGE(As1, Bs1, As2, Bs0)
+      GEMM_STAGE(As0, Bs0, As1, Bs1, As2)
+      GEMM_STAGE(As1, Bs1, As2, Bs0, As0)
     }
     if (kt + 2 <= KT) {
-      GEMM_STAGE(As2, Bs0, As0, Bs1)
-      GEMM_STAGE(As0, Bs1, As1, Bs0)
+      GEMM_STAGE(As2, Bs0, As0, Bs1, As1)
+      GEMM_STAGE(As0, Bs1, As1, Bs0, As2)
     }
 #undef GEMM_STAGE
   };
