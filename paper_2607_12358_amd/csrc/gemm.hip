@@ -6,18 +6,19 @@
 //   2 x 4 grid (two per SIMD), each wave 128 x 64 = 4 x 2 MFMA blocks of
 //   32 x 32.  Operands go global -> LDS directly (global_load_lds_dwordx4,
 //   no staging registers) into a ring of 32 KB operand tiles (three for
-//   the activations, fetched two K-steps ahead, two for the weights, one
-//   ahead: 160 KB, the whole LDS), K-contiguous 128-byte rows
+//   the activations, requested about 1.75 K-steps ahead, two for the
+//   weights, 1.25 ahead: 160 KB, the whole LDS), K-contiguous 128-byte rows
 //   (whole cache lines, so the L2 request rate stays within budget) with an
 //   XOR swizzle that is conflict-free for gfx950's 64 LDS banks.  One
 //   barrier per K-step, placed before the last 16-wide sub-step so the
-//   refill DMA and the next stage's first fragment reads hide behind its
-//   MFMAs; all other fragment reads are software-pipelined one sub-step
-//   ahead.  A wave that issues global loads holds back its own MFMA issue,
-//   so two waves share each SIMD and one of them issues the DMAs of both:
-//   the other only reads fragments and issues MFMAs.  A 256 x 256 tile halves the operand bytes per
-//   flop of a 256 x 128 tile (operand traffic also costs clock under the
-//   power cap).  The activation tile feeds MFMA operand A and the weight
+//   weight refill and the next stage's first fragment reads hide behind its
+//   MFMAs (the activation refill runs under the first sub-step); all other
+//   fragment reads are software-pipelined one sub-step ahead.  A wave that
+//   issues global loads holds back its own MFMA issue, so two waves share
+//   each SIMD and one of them issues the DMAs of both: the other only reads
+//   fragments and issues MFMAs.  A 256 x 256 tile halves the operand bytes
+//   per flop of a 256 x 128 tile (operand traffic also costs clock under
+//   the power cap).  The activation tile feeds MFMA operand A and the weight
 //   tile operand B, so the accumulator holds C with lanes along features:
 //   every epilogue store is a run of consecutive features of one token row
 //   (coalesced), and bias / gate are one value per lane.  Workgroups are
