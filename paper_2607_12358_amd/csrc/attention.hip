@@ -180,31 +180,40 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void attn_bf16_kernel(const bf16* 
   const uint32_t ks_lds = (uint32_t)(uintptr_t)(lds_void_t*)Ks;
   const uint32_t vs_lds = (uint32_t)(uintptr_t)(lds_void_t*)Vs;
 
-  // DMA staging of a full tile: instruction i of wave w fills 1 KB at
-  // (CPT w + i) KB of the tile.  K tile: LDS row r (D * 2 bytes) holds key
-  // j0 + key_perm(r); V^T tile: LDS row d (128 bytes) holds keys j0 .. j0+63
-  // of head dim d; chunks sit at swizzled slots (swz).  Per-lane byte offsets
-  // relative to the tile's first element:
-  uint32_t koff[CPT], voff[CPT];
+  // DMA staging of a full tile in 1 KB blocks: block b = CPT w + i is wave
+  // w's share.  K tile: LDS row r (D * 2 bytes) holds key j0 + key_perm(r);
+  // V^T tile: LDS row d (128 bytes) holds keys j0 .. j0+63 of head dim d;
+  // chunks sit at swizzled slots (swz).  With 8 waves (two per SIMD: waves
+  // w and w + 4) wave w issues the blocks of both, so wave w + 4 issues no
+  // global loads in the loop.  Per-lane byte offsets relative to the tile's
+  // first element, and the block each DMA fills:
+  constexpr bool kPairDma = NW == 8;
+  constexpr int NB = kPairDma ? 2 * CPT : CPT;
+  const bool dma_wave = !kPairDma || wave < 4;
+  uint32_t koff[NB], voff[NB];
+  int kblk[NB];
 #pragma unroll
-  for (int i = 0; i < CPT; ++i) {
-    const int blk = wave * CPT + i;
+  for (int i = 0; i < NB; ++i) {
+    const int blk = (kPairDma ? (wave & 3) + (i / CPT) * 4 : wave) * CPT + i % CPT;
+    kblk[i] = blk;
     const int r = blk * KROWS_PER_KB + lane / KCH;
     koff[i] = (uint32_t)(key_perm(r) * D + swz<KCH>(r, lane % KCH) * 8) * 2u;
     const int d = blk * 8 + (lane >> 3);
     voff[i] = (uint32_t)(d * vld + swz<8>(d, lane & 7) * 8) * 2u;
   }
   auto stage_k_dma = [&](int buf, int j0) {
+    if (!dma_wave) return;
     const uint64_t base = uniform_ptr(Kh + (int64_t)j0 * D);
 #pragma unroll
-    for (int i = 0; i < CPT; ++i)
-      dma16(base, koff[i], ks_lds + buf * Ld::K_ELEMS * 2 + (wave * CPT + i) * 1024);
+    for (int i = 0; i < NB; ++i)
+      dma16(base, koff[i], ks_lds + buf * Ld::K_ELEMS * 2 + kblk[i] * 1024);
   };
   auto stage_v_dma = [&](int buf, int j0) {
+    if (!dma_wave) return;
     const uint64_t base = uniform_ptr(Vh + j0);
 #pragma unroll
-    for (int i = 0; i < CPT; ++i)
-      dma16(base, voff[i], vs_lds + buf * Ld::V_ELEMS * 2 + (wave * CPT + i) * 1024);
+    for (int i = 0; i < NB; ++i)
+      dma16(base, voff[i], vs_lds + buf * Ld::V_ELEMS * 2 + kblk[i] * 1024);
   };
   // The ragged tile j0 .. L-1 through registers, keys >= L zeroed (K rows,
   // and V^T columns, whose padding past L may hold anything).
